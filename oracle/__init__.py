@@ -1,0 +1,125 @@
+"""CPU oracle for the (m,l)-TCU hot path -- TEST INFRASTRUCTURE ONLY.
+
+Only the tests, the smoke check and the benchmark's CPU-baseline leg use this
+package; the GPU library and its Python binding never import it.  It wraps
+``liboracle.so`` (built from ``tcu_oracle.c`` by ``oracle/build.py``) with
+numpy in/out:
+
+* ``mm(A, B, dtype, rows=None)`` -- the plain product ``C = A*B`` that both
+  the native tensor-unit call (Section 3, model definition) and the blocked
+  multiplication of Theorem 2 (Section 4.1) compute.  ``A`` and ``B`` hold the
+  stored bit patterns (uint16 for 'f16'/'bf16', int8 for 'i8'); the result is
+  float64 (floating point) or int64 (exact integer).  ``rows`` selects rows of
+  A so that large cases can be checked on sampled rows.
+* ``f16_to_f64``, ``bf16_to_f64`` -- format decoders.
+* ``f64_to_bf16`` -- one-step round-to-nearest-even to bfloat16 bit patterns.
+
+Every function here is pinned by tests/test_oracle_pins.py against values the
+mathematics fixes (exact rational brute force, closed forms, library
+routines on special cases); none is "parity unpinned".
+"""
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_DTYPES = {"f16": 0, "bf16": 1, "i8": 2}
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        from . import build as _build
+        _build.build()
+    lib = ctypes.CDLL(_LIB_PATH)
+    i64, vp = ctypes.c_int64, ctypes.c_void_p
+    lib.oracle_f16_to_f64.argtypes = [ctypes.c_uint16]
+    lib.oracle_f16_to_f64.restype = ctypes.c_double
+    lib.oracle_bf16_to_f64.argtypes = [ctypes.c_uint16]
+    lib.oracle_bf16_to_f64.restype = ctypes.c_double
+    lib.oracle_f64_to_bf16_rne.argtypes = [ctypes.c_double]
+    lib.oracle_f64_to_bf16_rne.restype = ctypes.c_uint16
+    lib.oracle_f64_to_bf16_array.argtypes = [vp, vp, i64]
+    lib.oracle_f64_to_bf16_array.restype = None
+    lib.oracle_decode_array.argtypes = [ctypes.c_int, vp, vp, i64]
+    lib.oracle_decode_array.restype = None
+    lib.oracle_mm_f64.argtypes = [ctypes.c_int, vp, vp, i64, i64, i64, vp, i64, vp]
+    lib.oracle_mm_f64.restype = ctypes.c_int
+    lib.oracle_mm_i64.argtypes = [vp, vp, i64, i64, i64, vp, i64, vp]
+    lib.oracle_mm_i64.restype = ctypes.c_int
+    lib.oracle_threads.argtypes = []
+    lib.oracle_threads.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _ptr(a: np.ndarray):
+    return ctypes.c_void_p(a.ctypes.data)
+
+
+def threads() -> int:
+    """OpenMP threads the oracle's loops use."""
+    return int(_load().oracle_threads())
+
+
+def decode(bits: np.ndarray, dtype: str) -> np.ndarray:
+    """Decode stored f16/bf16 bit patterns (uint16) or int8 values to float64."""
+    code = _DTYPES[dtype]
+    want = np.int8 if dtype == "i8" else np.uint16
+    bits = np.ascontiguousarray(bits).view(want)
+    out = np.empty(bits.shape, dtype=np.float64)
+    _load().oracle_decode_array(code, _ptr(bits), _ptr(out), bits.size)
+    return out
+
+
+def f16_to_f64(bits: np.ndarray) -> np.ndarray:
+    return decode(bits, "f16")
+
+
+def bf16_to_f64(bits: np.ndarray) -> np.ndarray:
+    return decode(bits, "bf16")
+
+
+def f64_to_bf16(x: np.ndarray) -> np.ndarray:
+    """Round float64 values to bfloat16 (RNE, one step); returns uint16 bits."""
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    out = np.empty(x.shape, dtype=np.uint16)
+    _load().oracle_f64_to_bf16_array(_ptr(x), _ptr(out), x.size)
+    return out
+
+
+def mm(A: np.ndarray, B: np.ndarray, dtype: str, rows=None) -> np.ndarray:
+    """C = A*B (selected rows of it) as float64, or int64 for dtype 'i8'.
+
+    A: (R, K) and B: (K, J) arrays of stored values: uint16 bit patterns for
+    'f16'/'bf16' (int16 views are accepted), int8 for 'i8'.
+    """
+    if A.ndim != 2 or B.ndim != 2 or A.shape[1] != B.shape[0]:
+        raise ValueError(f"shape mismatch: {A.shape} x {B.shape}")
+    R, K = A.shape
+    J = B.shape[1]
+    lib = _load()
+    if rows is None:
+        ids_ptr, n_ids = None, R
+    else:
+        ids = np.ascontiguousarray(rows, dtype=np.int64)
+        ids_ptr, n_ids = _ptr(ids), ids.size
+    if dtype == "i8":
+        a = np.ascontiguousarray(A).view(np.int8)
+        b = np.ascontiguousarray(B).view(np.int8)
+        out = np.empty((n_ids, J), dtype=np.int64)
+        rc = lib.oracle_mm_i64(_ptr(a), _ptr(b), R, K, J, ids_ptr, n_ids, _ptr(out))
+    else:
+        a = np.ascontiguousarray(A).view(np.uint16)
+        b = np.ascontiguousarray(B).view(np.uint16)
+        out = np.empty((n_ids, J), dtype=np.float64)
+        rc = lib.oracle_mm_f64(_DTYPES[dtype], _ptr(a), _ptr(b), R, K, J,
+                               ids_ptr, n_ids, _ptr(out))
+    if rc != 0:
+        raise ValueError("oracle rejected its arguments")
+    return out

@@ -1,0 +1,105 @@
+"""Seeded synthetic inputs shared by the tests, the smoke check and the benchmark.
+
+This module holds no arithmetic of the method: it only draws random matrices
+(and a few structured ones: identity, permutation, small integers) on the host
+and stores them in the dtype the tensor unit reads.  Both the GPU path and the
+CPU oracle are fed the *same bytes* produced here.
+
+Recipe (the paper has no datasets; every input is i.i.d. synthetic):
+  * a torch CPU ``Generator`` seeded with the workload's seed draws A first,
+    then B;
+  * floating-point matrices are drawn in float32 -- uniform on [-1, 1) as
+    ``2*rand - 1`` or standard normal -- and rounded once, to nearest-even,
+    to float16 / bfloat16;
+  * int8 matrices are drawn uniformly from {-128, ..., 127}.
+"""
+from __future__ import annotations
+
+import torch
+
+# Workloads of the hot path.  "tall": one native call, A (n x s) times
+# B (s x s).  "gemm": the blocked N x N product, unit size s.
+WORKLOADS = {
+    "tall_f16_n4096_s16": dict(kind="tall", dtype="f16", out="f32", n=4096, s=16,
+                               dist="uniform", seed=0),
+    "gemm_f16_N1024_s16": dict(kind="gemm", dtype="f16", out="f32", N=1024, s=16,
+                               dist="uniform", seed=1),
+    "gemm_bf16_N8192_s32": dict(kind="gemm", dtype="bf16", out="f32", N=8192, s=32,
+                                dist="normal", seed=2),
+    "gemm_i8_N8192_s32": dict(kind="gemm", dtype="i8", out="i32", N=8192, s=32,
+                              dist="int8", seed=3),
+    "tall_bf16_n16777216_s32": dict(kind="tall", dtype="bf16", out="bf16", n=1 << 24,
+                                    s=32, dist="normal", seed=4),
+}
+
+TORCH_DTYPE = {"f16": torch.float16, "bf16": torch.bfloat16, "i8": torch.int8,
+               "f32": torch.float32, "i32": torch.int32}
+
+
+def draw(shape, dtype: str, dist: str, gen: torch.Generator) -> torch.Tensor:
+    """One random matrix in storage dtype ``dtype`` ('f16', 'bf16', 'i8')."""
+    if dtype == "i8":
+        if dist not in ("int8", "uniform"):
+            raise ValueError(f"int8 inputs are drawn uniformly, not {dist!r}")
+        return torch.randint(-128, 128, shape, generator=gen, dtype=torch.int8)
+    if dist == "uniform":
+        x = torch.rand(shape, generator=gen, dtype=torch.float32).mul_(2.0).sub_(1.0)
+    elif dist == "normal":
+        x = torch.randn(shape, generator=gen, dtype=torch.float32)
+    elif dist == "smallint":
+        x = torch.randint(-2, 3, shape, generator=gen).to(torch.float32)
+    else:
+        raise ValueError(f"unknown distribution {dist!r}")
+    return x.to(TORCH_DTYPE[dtype])
+
+
+def shapes(spec: dict):
+    """(A shape, B shape, C shape) of a workload spec."""
+    if spec["kind"] == "tall":
+        n, s = spec["n"], spec["s"]
+        return (n, s), (s, s), (n, s)
+    N = spec["N"]
+    return (N, N), (N, N), (N, N)
+
+
+def make_inputs(spec: dict, seed: int | None = None):
+    """Draw (A, B) on the host for a workload spec: A first, then B."""
+    gen = torch.Generator(device="cpu")
+    gen.manual_seed(spec["seed"] if seed is None else seed)
+    a_shape, b_shape, _ = shapes(spec)
+    A = draw(a_shape, spec["dtype"], spec["dist"], gen)
+    B = draw(b_shape, spec["dtype"], spec["dist"], gen)
+    return A, B
+
+
+def small_ints(shape, dtype: str, seed: int) -> torch.Tensor:
+    """Integers in {-2..2} stored in ``dtype`` (exact in every storage type)."""
+    gen = torch.Generator(device="cpu")
+    gen.manual_seed(seed)
+    return torch.randint(-2, 3, shape, generator=gen).to(TORCH_DTYPE[dtype])
+
+
+def identity(s: int, dtype: str) -> torch.Tensor:
+    return torch.eye(s, dtype=torch.float32).to(TORCH_DTYPE[dtype])
+
+
+def permutation(s: int, dtype: str, seed: int):
+    """(P, perm) with P[perm[j], j] = 1, so (A P)[:, j] = A[:, perm[j]]."""
+    gen = torch.Generator(device="cpu")
+    gen.manual_seed(seed)
+    perm = torch.randperm(s, generator=gen)
+    P = torch.zeros(s, s, dtype=torch.float32)
+    P[perm, torch.arange(s)] = 1.0
+    return P.to(TORCH_DTYPE[dtype]), perm
+
+
+def bits(t: torch.Tensor):
+    """Stored bytes of a CPU tensor as a numpy array (uint16 for 16-bit
+    floats, int8 for int8) -- the form the oracle reads."""
+    import numpy as np
+    t = t.contiguous()
+    if t.dtype in (torch.float16, torch.bfloat16):
+        return t.view(torch.int16).numpy().view(np.uint16)
+    if t.dtype == torch.int8:
+        return t.numpy()
+    raise TypeError(f"no stored-bits view for {t.dtype}")

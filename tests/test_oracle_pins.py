@@ -1,0 +1,381 @@
+"""Pins of the CPU oracle against what the mathematics fixes (CPU only).
+
+Each oracle function is checked by a route that does not reuse its code:
+  * format decoders: exhaustively against numpy's float16 conversion and the
+    binary32 reinterpretation of a bfloat16 pattern;
+  * the bfloat16 rounding: against exact rational nearest-even search, torch's
+    binary32 -> bfloat16 conversion on binary32-exact inputs, and hand-derived
+    boundary cases (tests/golden/bf16_rne_cases.txt);
+  * the product C = A*B (what the native call of the model definition in
+    Section 3 and the blocked multiplication of Theorem 2 compute): exact
+    rational / integer brute force on tiny inputs, numpy's int64 and float64
+    matmul, identity and permutation right operands, closed forms with
+    non-symmetric operands, and small-integer inputs whose sums are exact.
+A last group plants plausible mistakes in the oracle (transposed operand,
+dropped term, shifted index, wrong sign) and checks that the pins catch them.
+"""
+import os
+import struct
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import torch
+
+from paper_1908_06649_amd import inputs
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+# ------------------------------------------------------------------ helpers
+def f16_exact(bits16: int) -> Fraction:
+    return Fraction(struct.unpack("<e", struct.pack("<H", bits16))[0])
+
+
+def bf16_exact(bits16: int) -> Fraction:
+    return Fraction(struct.unpack("<f", struct.pack("<I", bits16 << 16))[0])
+
+
+def exact_mm(A_bits, B_bits, dtype):
+    """Exact product with Python rationals / ints (brute force)."""
+    R, K = A_bits.shape
+    J = B_bits.shape[1]
+    if dtype == "i8":
+        a = [[int(x) for x in row] for row in A_bits]
+        b = [[int(x) for x in row] for row in B_bits]
+    else:
+        dec = f16_exact if dtype == "f16" else bf16_exact
+        a = [[dec(int(x)) for x in row] for row in A_bits]
+        b = [[dec(int(x)) for x in row] for row in B_bits]
+    return [[sum(a[r][k] * b[k][j] for k in range(K)) for j in range(J)] for r in range(R)]
+
+
+def abs_mm(A_bits, B_bits, dtype):
+    """|A| |B| via numpy on independently decoded values."""
+    a, b = np_decode(A_bits, dtype), np_decode(B_bits, dtype)
+    return np.abs(a) @ np.abs(b)
+
+
+def np_decode(bits, dtype):
+    if dtype == "f16":
+        return np.asarray(bits, dtype=np.uint16).view(np.float16).astype(np.float64)
+    if dtype == "bf16":
+        u32 = np.asarray(bits, dtype=np.uint16).astype(np.uint32) << 16
+        return u32.view(np.float32).astype(np.float64)
+    return np.asarray(bits, dtype=np.int8).astype(np.float64)
+
+
+def gen_bits(shape, dtype, dist, seed):
+    g = torch.Generator().manual_seed(seed)
+    return inputs.bits(inputs.draw(shape, dtype, dist, g))
+
+
+# ------------------------------------------------------------- decoders
+def test_f16_decode_exhaustive(oracle_mod):
+    allbits = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    got = oracle_mod.f16_to_f64(allbits)
+    ref = allbits.view(np.float16).astype(np.float64)
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(got), nan)
+    assert np.array_equal(got[~nan], ref[~nan])
+    assert np.array_equal(np.signbit(got[~nan]), np.signbit(ref[~nan]))
+
+
+def test_bf16_decode_exhaustive(oracle_mod):
+    allbits = np.arange(65536, dtype=np.uint32)
+    got = oracle_mod.bf16_to_f64(allbits.astype(np.uint16))
+    ref = (allbits << 16).view(np.float32).astype(np.float64)
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(got), nan)
+    assert np.array_equal(got[~nan], ref[~nan])
+    assert np.array_equal(np.signbit(got[~nan]), np.signbit(ref[~nan]))
+
+
+# ------------------------------------------------------------ bf16 encoder
+_POS_FINITE = np.arange(0x7F80, dtype=np.uint32)            # +0 .. max finite
+_POS_VALUES = [bf16_exact(int(b)) for b in _POS_FINITE]
+
+
+def exact_nearest_bf16(x: Fraction) -> int:
+    """Nearest bfloat16 to the rational x, ties to even; overflow to inf."""
+    sign = 0x8000 if x < 0 else 0
+    ax = -x if x < 0 else x
+    lo, hi = 0, len(_POS_VALUES) - 1
+    if ax >= _POS_VALUES[hi]:
+        top = _POS_VALUES[hi]
+        ulp = top - _POS_VALUES[hi - 1]
+        # beyond max finite: inf once |x| >= max + ulp/2 (the tie goes to the
+        # even neighbour 2^128, which is not finite)
+        return sign | (0x7F80 if ax >= top + ulp / 2 else 0x7F7F)
+    while hi - lo > 1:
+        mid = (lo + hi) // 2
+        if _POS_VALUES[mid] <= ax:
+            lo = mid
+        else:
+            hi = mid
+    dlo, dhi = ax - _POS_VALUES[lo], _POS_VALUES[hi] - ax
+    if dlo < dhi:
+        pick = lo
+    elif dhi < dlo:
+        pick = hi
+    else:
+        pick = lo if lo % 2 == 0 else hi
+    return sign | pick
+
+
+def test_bf16_rne_golden_cases(oracle_mod):
+    """Hand-derived boundary cases, one per line with its reasoning."""
+    n = 0
+    with open(os.path.join(GOLDEN, "bf16_rne_cases.txt")) as fh:
+        for line in fh:
+            line = line.split("#", 1)[0].strip()
+            if not line:
+                continue
+            xs, want = line.split()
+            x = float.fromhex(xs)
+            got = int(oracle_mod.f64_to_bf16(np.array([x]))[0])
+            assert got == int(want, 16), f"{xs}: got {got:#06x}, want {want}"
+            n += 1
+    assert n >= 20
+
+
+def test_bf16_rne_vs_exact_rational(oracle_mod):
+    """Random binary64 values (not binary32-exact) against exact search."""
+    rng = np.random.default_rng(1234)
+    mant = rng.uniform(1.0, 2.0, 600)
+    expo = rng.integers(-140, 129, 600)
+    sign = rng.choice([-1.0, 1.0], 600)
+    x = sign * np.ldexp(mant, expo)
+    # force exact ties and near-ties of bf16 at many binades
+    e2 = rng.integers(-126, 127, 200)
+    frac = rng.integers(0, 128, 200)
+    ties = np.ldexp((128.0 + frac + 0.5), e2 - 7)
+    near = np.nextafter(ties, np.inf)
+    x = np.concatenate([x, ties, near, -ties, np.nextafter(ties, 0)])
+    got = oracle_mod.f64_to_bf16(x)
+    for xi, gi in zip(x, got):
+        assert int(gi) == exact_nearest_bf16(Fraction(float(xi))), float(xi).hex()
+
+
+def test_bf16_rne_vs_torch_on_f32_exact(oracle_mod):
+    """On binary32-representable inputs one-step RNE equals torch's
+    binary32 -> bfloat16 conversion (also round-to-nearest-even)."""
+    rng = np.random.default_rng(7)
+    u = rng.integers(0, 1 << 32, 200000, dtype=np.uint64).astype(np.uint32)
+    f = u.view(np.float32)
+    f = f[np.isfinite(f)]
+    got = oracle_mod.f64_to_bf16(f.astype(np.float64))
+    ref = torch.from_numpy(f.copy()).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(got, ref)
+
+
+def test_bf16_rne_specials(oracle_mod):
+    x = np.array([np.inf, -np.inf, np.nan, 0.0, -0.0])
+    got = oracle_mod.f64_to_bf16(x)
+    assert got[0] == 0x7F80 and got[1] == 0xFF80
+    assert (got[2] & 0x7F80) == 0x7F80 and (got[2] & 0x7F) != 0
+    assert got[3] == 0x0000 and got[4] == 0x8000
+
+
+# ----------------------------------------------------------------- product
+TINY = [(s, n) for s in (1, 2, 4, 16, 32) for n in (s, s + 1, 2 * s + 3)]
+
+
+@pytest.mark.parametrize("dtype", ["f16", "bf16"])
+@pytest.mark.parametrize("s,n", TINY)
+def test_mm_vs_exact_rational(oracle_mod, dtype, s, n):
+    dist = "uniform" if dtype == "f16" else "normal"
+    A = gen_bits((n, s), dtype, dist, 100 + s + n)
+    B = gen_bits((s, s), dtype, dist, 200 + s + n)
+    got = oracle_mod.mm(A, B, dtype)
+    ex = exact_mm(A, B, dtype)
+    absab = abs_mm(A, B, dtype)
+    u = 2.0 ** -53
+    gam = s * u / (1 - s * u)
+    for r in range(n):
+        for j in range(s):
+            err = abs(Fraction(float(got[r, j])) - ex[r][j])
+            assert err <= Fraction(gam) * Fraction(float(absab[r, j])) + Fraction(2.0 ** -1074)
+
+
+@pytest.mark.parametrize("s,n", TINY)
+def test_mm_int8_vs_exact_int(oracle_mod, s, n):
+    A = gen_bits((n, s), "i8", "int8", 300 + s + n)
+    B = gen_bits((s, s), "i8", "int8", 400 + s + n)
+    got = oracle_mod.mm(A, B, "i8")
+    assert got.tolist() == exact_mm(A, B, "i8")
+
+
+def test_mm_int8_vs_numpy_int64(oracle_mod):
+    A = gen_bits((97, 64), "i8", "int8", 5)
+    B = gen_bits((64, 48), "i8", "int8", 6)
+    ref = A.astype(np.int64) @ B.astype(np.int64)
+    assert np.array_equal(oracle_mod.mm(A, B, "i8"), ref)
+
+
+@pytest.mark.parametrize("dtype", ["f16", "bf16"])
+def test_mm_vs_numpy_f64(oracle_mod, dtype):
+    A = gen_bits((83, 256), dtype, "normal", 8)
+    B = gen_bits((256, 64), dtype, "normal", 9)
+    ref = np_decode(A, dtype) @ np_decode(B, dtype)
+    bound = 256 * 2.0 ** -52 * abs_mm(A, B, dtype)
+    assert np.all(np.abs(oracle_mod.mm(A, B, dtype) - ref) <= bound)
+
+
+@pytest.mark.parametrize("dtype", ["f16", "bf16", "i8"])
+@pytest.mark.parametrize("s", [16, 32])
+def test_mm_identity(oracle_mod, dtype, s):
+    dist = "int8" if dtype == "i8" else "normal"
+    A = gen_bits((3 * s + 5, s), dtype, dist, 11)
+    eye = inputs.bits(inputs.identity(s, dtype))
+    got = oracle_mod.mm(A, eye, dtype)
+    assert np.array_equal(got, np_decode(A, dtype).astype(got.dtype))
+    if dtype == "bf16":       # the one-step bf16 output of an exact value is the value
+        assert np.array_equal(oracle_mod.f64_to_bf16(got), A)
+
+
+@pytest.mark.parametrize("dtype", ["f16", "bf16", "i8"])
+def test_mm_permutation(oracle_mod, dtype):
+    s = 32
+    dist = "int8" if dtype == "i8" else "uniform"
+    A = gen_bits((77, s), dtype, dist, 12)
+    P, perm = inputs.permutation(s, dtype, 13)
+    got = oracle_mod.mm(A, inputs.bits(P), dtype)
+    want = np_decode(A, dtype)[:, perm.numpy()]
+    assert np.array_equal(got, want.astype(got.dtype))
+
+
+def _closed_form_operands(R, K, J, dtype):
+    """A[r][k] = r + 2k - 40 and B[k][j] = k - j + 3: non-symmetric, small
+    integers exact in every storage type for R, K, J <= 32."""
+    r = np.arange(R)[:, None]
+    k = np.arange(K)[None, :]
+    A = (r + 2 * k - 40).astype(np.float32)
+    kk = np.arange(K)[:, None]
+    j = np.arange(J)[None, :]
+    B = (kk - j + 3).astype(np.float32)
+    to = inputs.TORCH_DTYPE[dtype]
+    return inputs.bits(torch.from_numpy(A).to(to)), inputs.bits(torch.from_numpy(B).to(to))
+
+
+def _closed_form_value(R, K, J):
+    # sum_k (r + 2k - 40)(k - j + 3) = (r-40)(S1 + K(3-j)) + 2(S2 + (3-j) S1)
+    S1 = K * (K - 1) // 2
+    S2 = (K - 1) * K * (2 * K - 1) // 6
+    r = np.arange(R)[:, None]
+    j = np.arange(J)[None, :]
+    return (r - 40) * (S1 + K * (3 - j)) + 2 * (S2 + (3 - j) * S1)
+
+
+def check_closed_form(mm_fn, dtype):
+    """Pins used for the oracle and for the planted mistakes below."""
+    for (R, K, J) in [(32, 32, 32), (19, 16, 16), (5, 7, 3)]:
+        A, B = _closed_form_operands(R, K, J, dtype)
+        got = mm_fn(A, B, dtype)
+        if not np.array_equal(np.asarray(got, dtype=np.float64),
+                              _closed_form_value(R, K, J).astype(np.float64)):
+            return False
+    return True
+
+
+@pytest.mark.parametrize("dtype", ["f16", "bf16", "i8"])
+def test_mm_closed_form(oracle_mod, dtype):
+    assert check_closed_form(oracle_mod.mm, dtype)
+
+
+def test_mm_ones(oracle_mod):
+    for dtype in ("f16", "bf16", "i8"):
+        ones = inputs.bits(torch.ones(40, 32).to(inputs.TORCH_DTYPE[dtype]))
+        onesB = inputs.bits(torch.ones(32, 32).to(inputs.TORCH_DTYPE[dtype]))
+        assert np.all(oracle_mod.mm(ones, onesB, dtype) == 32)
+
+
+@pytest.mark.parametrize("dtype", ["f16", "bf16", "i8"])
+def test_mm_small_ints_exact(oracle_mod, dtype):
+    A = inputs.bits(inputs.small_ints((130, 96), dtype, 21))
+    B = inputs.bits(inputs.small_ints((96, 80), dtype, 22))
+    ref = np_decode(A, dtype).astype(np.int64) @ np_decode(B, dtype).astype(np.int64)
+    assert np.array_equal(np.asarray(oracle_mod.mm(A, B, dtype), dtype=np.float64),
+                          ref.astype(np.float64))
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "i8"])
+def test_mm_row_subset(oracle_mod, dtype):
+    dist = "int8" if dtype == "i8" else "normal"
+    A = gen_bits((200, 64), dtype, dist, 31)
+    B = gen_bits((64, 64), dtype, dist, 32)
+    full = oracle_mod.mm(A, B, dtype)
+    rows = np.array([199, 0, 57, 57, 123])
+    assert np.array_equal(oracle_mod.mm(A, B, dtype, rows=rows), full[rows])
+
+
+def test_mm_rejects_bad_rows(oracle_mod):
+    A = gen_bits((8, 16), "bf16", "normal", 1)
+    B = gen_bits((16, 16), "bf16", "normal", 2)
+    with pytest.raises(ValueError):
+        oracle_mod.mm(A, B, "bf16", rows=np.array([8]))
+    with pytest.raises(ValueError):
+        oracle_mod.mm(A, B[:8], "bf16")
+
+
+# ------------------------------------------- structure of Theorem 2 / weak model
+def test_blocked_composition_equals_product(oracle_mod):
+    """Theorem 2 (Section 4.1): with A split into N x s vertical strips A_i and
+    B into s x s blocks B_{i,j}, output strip j is sum_i A_i B_{i,j}
+    (the reading of the summation index that yields A*B)."""
+    N, s = 96, 16
+    A = gen_bits((N, N), "i8", "int8", 41)
+    B = gen_bits((N, N), "i8", "int8", 42)
+    full = oracle_mod.mm(A, B, "i8")
+    nb = N // s
+    calls = 0
+    C = np.zeros((N, N), dtype=np.int64)
+    for i in range(nb):
+        Ai = np.ascontiguousarray(A[:, i * s:(i + 1) * s])
+        for j in range(nb):
+            Bij = np.ascontiguousarray(B[i * s:(i + 1) * s, j * s:(j + 1) * s])
+            C[:, j * s:(j + 1) * s] += oracle_mod.mm(Ai, Bij, "i8")
+            calls += 1
+    assert calls == (N // s) ** 2          # n/m calls, n = N^2, m = s^2
+    assert np.array_equal(C, full)
+
+
+def test_weak_model_stacked_square_calls(oracle_mod):
+    """Section 5: a tall n x s call equals n/s stacked s x s calls."""
+    s, n = 32, 32 * 9
+    A = gen_bits((n, s), "i8", "int8", 51)
+    B = gen_bits((s, s), "i8", "int8", 52)
+    tall = oracle_mod.mm(A, B, "i8")
+    stacked = np.concatenate([oracle_mod.mm(np.ascontiguousarray(A[q * s:(q + 1) * s]), B, "i8")
+                              for q in range(n // s)])
+    assert np.array_equal(tall, stacked)
+
+
+# ------------------------------------------------------- planted mistakes
+def _mutants(oracle_mod):
+    def transposed_b(A, B, dt):
+        return oracle_mod.mm(A, np.ascontiguousarray(B.T), dt) if B.shape[0] == B.shape[1] else None
+
+    def dropped_last_term(A, B, dt):
+        return oracle_mod.mm(np.ascontiguousarray(A[:, :-1]), np.ascontiguousarray(B[:-1]), dt)
+
+    def shifted_row(A, B, dt):
+        return np.roll(oracle_mod.mm(A, B, dt), 1, axis=0)
+
+    def negated_b(A, B, dt):
+        return -oracle_mod.mm(A, B, dt)
+
+    def swapped_operands(A, B, dt):
+        if A.shape[0] != A.shape[1] or B.shape[0] != B.shape[1]:
+            return None
+        return oracle_mod.mm(B, A, dt)
+
+    return [transposed_b, dropped_last_term, shifted_row, negated_b, swapped_operands]
+
+
+def test_pins_catch_planted_mistakes(oracle_mod):
+    for mut in _mutants(oracle_mod):
+        def fn(A, B, dt, mut=mut):
+            out = mut(A, B, dt)
+            return np.full((A.shape[0], B.shape[1]), np.nan) if out is None else out
+        assert not check_closed_form(fn, "i8"), mut.__name__
