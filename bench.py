@@ -1,0 +1,327 @@
+#!/usr/bin/env python3
+"""Benchmark of the (m,l)-TCU hot path on one MI355X.
+
+One step is one tcu_gemm call on the headline workload (the blocked product
+of Theorem 2, which performs every stage of the path: weights loaded into the
+unit, tall strips streamed through it, partial products summed, output
+written, calls counted), with inputs already resident in HBM.  Prints ONE
+JSON line:
+
+  value      TFLOP/s of tcu_gemm on gemm_bf16_N8192_s32 (A, B 8192 x 8192
+             bfloat16 ~ N(0,1), seed 2; unit s = 32; binary32 sums/output)
+  roofline   that kernel against the dense bf16 matrix-core peak, with the
+             HBM traffic rocprofv3 counted for it (when still current)
+  cpu_baseline  the CPU oracle timed on a bounded sample of the same product
+             on this host's cores, and the sampled rows' parity
+  secondary  the other workloads measured the same way: the very tall
+             bf16 native call (GB/s vs HBM peak), the int8 product (TOP/s),
+             the 4096 x 16 native call and the N = 1024 fp16 product
+  cost_model calls issued vs Theorem 2's count and bound, weak-model square
+             calls, model work, and the per-call latency l fitted as the
+             intercept of t(n) = a*n + l for native calls
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+       [--no-cpu-baseline] [--no-secondary] [--copy-probe]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = ("TFLOP/s (or TOP/s) and % MFMA peak for tcu_gemm; "
+          "GB/s and % HBM peak for tcu_mm_tall")
+HEADLINE = "gemm_bf16_N8192_s32"
+# MI355X published peaks (dense): matrix cores by input type, and HBM3E.
+PEAK = {"f16": 2500.0, "bf16": 2500.0, "i8": 5000.0}   # TFLOP/s or TOP/s
+HBM_PEAK_GBS = 8000.0
+CSRC = os.path.join(ROOT, "paper_1908_06649_amd", "csrc")
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def kernel_sources(kind: str):
+    main = "tcu_gemm.hip" if kind == "gemm" else "tcu_tall.hip"
+    return [os.path.join(CSRC, f) for f in (main, "tcu_device.h")]
+
+
+def kernel_hash(kind: str) -> str:
+    h = hashlib.sha256()
+    for p in kernel_sources(kind):
+        with open(p, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def counted_traffic(name: str, kind: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary of
+    this workload, if it was taken on the current kernel source; else None."""
+    path = os.path.join(PROFILES, f"{name}_counters.txt")
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    with open(path) as fh:
+        for line in fh:
+            m = re.match(r"^([a-z_0-9]+):\s*(\S+)", line.strip())
+            if m:
+                fields[m.group(1)] = m.group(2)
+    if fields.get("kernel_source_sha256") != kernel_hash(kind):
+        return None
+    try:
+        return float(fields["hbm_bytes_per_dispatch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def algorithmic(spec: dict):
+    """(work per call in flop/op, bytes per call) that the method must do."""
+    from paper_1908_06649_amd import inputs
+    ib = 1 if spec["dtype"] == "i8" else 2
+    ob = 2 if spec["out"] == "bf16" else 4
+    if spec["kind"] == "tall":
+        n, s = spec["n"], spec["s"]
+        return 2.0 * n * s * s, n * s * ib + s * s * ib + n * s * ob
+    N = spec["N"]
+    del inputs
+    return 2.0 * N ** 3, 2 * N * N * ib + N * N * ob
+
+
+class Workload:
+    """Inputs of one workload resident on the device, plus the call."""
+
+    def __init__(self, name: str):
+        import torch
+        from paper_1908_06649_amd import inputs, tcu
+        self.name, self.spec = name, inputs.WORKLOADS[name]
+        self.tcu = tcu
+        self.A, self.B = inputs.make_inputs(self.spec)
+        self.dA, self.dB = self.A.cuda(), self.B.cuda()
+        _, _, c_shape = inputs.shapes(self.spec)
+        self.C = torch.empty(c_shape, dtype=inputs.TORCH_DTYPE[self.spec["out"]], device="cuda")
+        self.s = self.spec["s"]
+
+    def call(self):
+        sp = self.spec
+        if sp["kind"] == "gemm":
+            self.tcu.tcu_gemm(self.dA, self.dB, self.C, sp["N"])
+        else:
+            self.tcu.tcu_mm_tall(self.dA, sp["n"], sp["s"], self.dB, self.C)
+
+
+def time_steps(fn, steps: int, warmup: int) -> float:
+    """Average ms per call over `steps` back-to-back calls, timed with HIP
+    events on the current stream (the stream the library launches on)."""
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    st = torch.cuda.current_stream()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(st)
+    for _ in range(steps):
+        fn()
+    e1.record(st)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps
+
+
+def measure(name: str, steps: int, warmup: int) -> dict:
+    w = Workload(name)
+    tcu = w.tcu
+    tcu.tcu_set_unit(w.s)
+    ms = time_steps(w.call, steps, warmup)
+    tcu.tcu_reset_calls()
+    w.call()
+    import torch
+    torch.cuda.synchronize()
+    calls, squares, work = tcu.tcu_calls(), tcu.tcu_square_calls(), tcu.tcu_work()
+    flops, nbytes = algorithmic(w.spec)
+    sp = w.spec
+    kind = sp["kind"]
+    out = {"workload": name, "ms_per_call": ms, "calls": calls, "square_calls": squares,
+           "model_work": work}
+    if kind == "gemm":
+        tput = flops / (ms * 1e-3) / 1e12
+        peak = PEAK[sp["dtype"]]
+        out.update({"value": tput, "unit": "TOP/s" if sp["dtype"] == "i8" else "TFLOP/s",
+                    "roofline": {"bound": "mfma", "achieved": tput, "peak": peak,
+                                 "unit": "TOP/s" if sp["dtype"] == "i8" else "TFLOP/s",
+                                 "frac": tput / peak,
+                                 "traffic": counted_traffic(name, kind)},
+                    "calls_theorem2": (sp["N"] // sp["s"]) ** 2,
+                    "algorithmic_flops": flops, "compulsory_bytes": nbytes})
+    else:
+        gbs = nbytes / (ms * 1e-3) / 1e9
+        out.update({"value": gbs, "unit": "GB/s",
+                    "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS,
+                                 "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS,
+                                 "traffic": counted_traffic(name, kind)},
+                    "tflops": flops / (ms * 1e-3) / 1e12,
+                    "algorithmic_bytes": nbytes, "algorithmic_flops": flops})
+    out["_workload"] = w
+    return out
+
+
+def ell_fit(steps: int = 200) -> dict:
+    """Per-call latency l: least-squares intercept of t(n) = a*n + l over
+    native bf16 -> bf16 calls with s = 32 (the model's O(n sqrt(m) + l))."""
+    import numpy as np
+    import torch
+    from paper_1908_06649_amd import tcu
+    s = 32
+    ns = [32, 1024, 4096, 16384, 65536, 262144, 1048576]
+    A = torch.randn(ns[-1], s, device="cuda").to(torch.bfloat16)
+    B = torch.randn(s, s, device="cuda").to(torch.bfloat16)
+    C = torch.empty(ns[-1], s, device="cuda", dtype=torch.bfloat16)
+    tcu.tcu_set_unit(s)
+    ts = []
+    for n in ns:
+        a, c = A[:n], C[:n]
+        ts.append(time_steps(lambda: tcu.tcu_mm_tall(a, n, s, B, c), steps, 10) * 1e3)
+    slope, icpt = np.polyfit(np.array(ns, dtype=float), np.array(ts), 1)
+    return {"n": ns, "us_per_call": [round(t, 3) for t in ts],
+            "fit_us_per_row": float(slope), "ell_us": float(icpt)}
+
+
+def cpu_baseline(w: "Workload", target_s: float = 15.0) -> dict:
+    """Time the CPU oracle on a bounded sample of the headline product:
+    R of the N output rows (2*R*N^2 flops), R sized for ~target_s seconds.
+    The sampled rows are also compared with the GPU result."""
+    import numpy as np
+    import oracle
+    from oracle import compare
+    from paper_1908_06649_amd import inputs
+    sp = w.spec
+    N, dt = sp["N"], sp["dtype"]
+    Ab, Bb = inputs.bits(w.A), inputs.bits(w.B)
+    rng = np.random.default_rng(123)
+    probe = np.sort(rng.choice(N, 4, replace=False))
+    t0 = time.perf_counter()
+    oracle.mm(Ab, Bb, dt, rows=probe)
+    per_row = (time.perf_counter() - t0) / len(probe)
+    R = int(max(8, min(N, target_s / max(per_row, 1e-9))))
+    rows = np.sort(rng.choice(N, R, replace=False))
+    t0 = time.perf_counter()
+    ref = oracle.mm(Ab, Bb, dt, rows=rows)
+    secs = time.perf_counter() - t0
+    got = w.C[rows].cpu()
+    got = got.view(np.int16) if False else got.numpy()
+    if dt == "i8":
+        parity = compare.check_exact(got, ref)
+    else:
+        absab = oracle.mm(compare.abs_bits(Ab), compare.abs_bits(Bb), dt, rows=rows)
+        parity = compare.check_float(got, ref, absab)
+    flops = 2.0 * R * N * N
+    return {"value": flops / secs / 1e12, "unit": "TOP/s" if dt == "i8" else "TFLOP/s",
+            "cores": oracle.threads(), "kind": "oracle",
+            "sample": f"{R} of {N} output rows of the {N}x{N} {dt} product "
+                      f"({flops:.3e} flop), binary64/int64 triple loop",
+            "seconds": secs, "parity_sampled_rows": parity}
+
+
+def copy_probe() -> None:
+    """A plain device copy of known size (1 GiB), for calibrating rocprofv3's
+    FETCH_SIZE / WRITE_SIZE counters."""
+    import torch
+    nbytes = 1 << 30
+    src = torch.empty(nbytes // 4, dtype=torch.int32, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes_each_way": nbytes, "copies": 3}))
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default=HEADLINE)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-secondary", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
+              "the hot path needs no collectives, and a multi-GPU run is not part of it.",
+              file=sys.stderr)
+        return 2
+    import torch
+    if not torch.cuda.is_available():
+        print("bench.py: no HIP device visible", file=sys.stderr)
+        return 2
+    from paper_1908_06649_amd import inputs, tcu
+    tcu.lib()   # raises if the HIP library is missing: no fallback
+    if args.copy_probe:
+        copy_probe()
+        return 0
+    if args.workload not in inputs.WORKLOADS:
+        print(f"unknown workload {args.workload}; choose from {sorted(inputs.WORKLOADS)}",
+              file=sys.stderr)
+        return 2
+
+    main_res = measure(args.workload, args.steps, args.warmup)
+    w = main_res.pop("_workload")
+    sp = w.spec
+    result = {
+        "metric": METRIC,
+        "value": main_res["value"],
+        "unit": main_res["unit"],
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": main_res["ms_per_call"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": sp["dtype"],
+        "data": "synthetic (seeded i.i.d. matrices; the paper has no datasets)",
+        "config": {"workload": args.workload,
+                   **{k: sp[k] for k in ("kind", "N", "n", "s") if k in sp},
+                   "dtype_in": sp["dtype"], "dtype_out": sp["out"],
+                   "distribution": sp["dist"], "seed": sp["seed"]},
+        "roofline": main_res["roofline"],
+    }
+    cost = {k: main_res[k] for k in ("calls", "square_calls", "model_work") if k in main_res}
+    if sp["kind"] == "gemm":
+        cost["calls_theorem2_and_lower_bound"] = main_res["calls_theorem2"]
+    if not args.no_cpu_baseline and sp["kind"] == "gemm":
+        result["cpu_baseline"] = cpu_baseline(w)
+    else:
+        result["cpu_baseline"] = None
+    del w
+    torch.cuda.empty_cache()
+
+    if not args.no_secondary:
+        sec = {}
+        for name in inputs.WORKLOADS:
+            if name == args.workload:
+                continue
+            spec = inputs.WORKLOADS[name]
+            steps = args.steps if spec.get("N", 0) >= 8192 or spec.get("n", 0) >= 1 << 20 else 200
+            r = measure(name, steps, max(args.warmup, 5))
+            r.pop("_workload")
+            sec[name] = {k: r[k] for k in ("value", "unit", "ms_per_call", "roofline", "calls",
+                                           "square_calls", "model_work")}
+            torch.cuda.empty_cache()
+        result["secondary"] = sec
+        cost["ell_fit"] = ell_fit()
+    result["cost_model"] = cost
+    result["kernel_source_sha256"] = {"gemm": kernel_hash("gemm"), "tall": kernel_hash("tall")}
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

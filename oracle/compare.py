@@ -1,0 +1,108 @@
+"""Parity checks of GPU results against the oracle -- TEST INFRASTRUCTURE ONLY.
+
+Tolerances (the paper fixes no precision; these are the stated bar):
+  * floating point: relative Frobenius error <= 1e-3 AND, elementwise,
+    |err_ij| <= 1e-2 * (|A| |B|)_ij, against the binary64 oracle;
+  * bfloat16 output: relative Frobenius error <= 1e-3 against the oracle
+    rounded once (nearest-even) to bfloat16 -- against the unrounded oracle
+    the output format alone costs about 1.7e-3 on N(0,1) data -- and the
+    elementwise bound above against the unrounded binary64 oracle (bfloat16
+    rounding alone is at most 2^-9 |c|).  In addition every element g must
+    be a nearest rounding of some value within the binary32 summation bound
+    of the exact sum s:  |g - s| <= ulp(g)/2 + K 2^-23 (|A| |B|)_ij, which
+    catches a wrong rounding step (truncation, double rounding across
+    binades) while allowing the legitimate one-step differences that
+    cancellation in a K-term binary32 sum produces;
+  * int8 -> int32: bit-exact.
+(|A| |B|) is the oracle's product of the operands with their sign bits
+cleared.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from . import f64_to_bf16, bf16_to_f64, mm
+
+REL_FROB = 1e-3
+ELEM = 1e-2
+
+
+def abs_bits(x: np.ndarray) -> np.ndarray:
+    """|x| of 16-bit float bit patterns (sign bit cleared)."""
+    return np.ascontiguousarray(x).view(np.uint16) & np.uint16(0x7FFF)
+
+
+def float_report(got: np.ndarray, ref: np.ndarray, absab: np.ndarray) -> dict:
+    got = np.asarray(got, dtype=np.float64)
+    err = np.abs(got - ref)
+    denom = np.linalg.norm(ref)
+    rel = float(np.linalg.norm(got - ref) / denom) if denom > 0 else float(np.linalg.norm(got - ref))
+    with np.errstate(divide="ignore", invalid="ignore"):
+        ratio = np.where(absab > 0, err / absab, np.where(err > 0, np.inf, 0.0))
+    return {"rel_frob": rel, "max_elem_ratio": float(ratio.max(initial=0.0)),
+            "max_abs_err": float(err.max(initial=0.0))}
+
+
+def check_float(got, ref, absab) -> dict:
+    rep = float_report(got, ref, absab)
+    assert rep["rel_frob"] <= REL_FROB, rep
+    assert rep["max_elem_ratio"] <= ELEM, rep
+    return rep
+
+
+def bf16_ulp_distance(a_bits: np.ndarray, b_bits: np.ndarray) -> np.ndarray:
+    """Distance in bfloat16 steps between two arrays of finite bf16 patterns."""
+    def ordered(x):
+        x = np.asarray(x, dtype=np.uint16).astype(np.int64)
+        mag = x & 0x7FFF
+        return np.where(x & 0x8000, -mag, mag)
+    return np.abs(ordered(a_bits) - ordered(b_bits))
+
+
+def bf16_spacing(x: np.ndarray) -> np.ndarray:
+    """Gap between consecutive bfloat16 values in the binade of |x|."""
+    ax = np.abs(np.asarray(x, dtype=np.float64))
+    e = np.floor(np.log2(np.where(ax > 0, ax, 1.0)))
+    e = np.maximum(e, -126.0)
+    return np.where(ax > 0, np.ldexp(1.0, (e - 7).astype(np.int64)), 2.0 ** -133)
+
+
+def check_bf16(got_bits, ref64, absab, K: int) -> dict:
+    got_bits = np.asarray(got_bits).view(np.uint16)
+    ref_bits = f64_to_bf16(ref64)
+    ulps = bf16_ulp_distance(got_bits, ref_bits)
+    got = bf16_to_f64(got_bits)
+    rounded = bf16_to_f64(ref_bits)
+    rep_r = float_report(got, rounded, absab)
+    rep_u = float_report(got, ref64, absab)
+    slack = np.abs(got - ref64) - (0.5 * bf16_spacing(got) + K * 2.0 ** -23 * absab)
+    rep = {"max_ulps_vs_rounded": int(ulps.max(initial=0)),
+           "frac_off_by_one": float((ulps > 0).mean()) if ulps.size else 0.0,
+           "rel_frob_vs_rounded": rep_r["rel_frob"],
+           "rel_frob_vs_unrounded": rep_u["rel_frob"],
+           "max_elem_ratio_vs_unrounded": rep_u["max_elem_ratio"],
+           "rounding_violations": int((slack > 0).sum())}
+    assert np.all(np.isfinite(got)), rep
+    assert rep["rounding_violations"] == 0, rep
+    assert rep["rel_frob_vs_rounded"] <= REL_FROB, rep
+    assert rep["max_elem_ratio_vs_unrounded"] <= ELEM, rep
+    return rep
+
+
+def check_exact(got, ref) -> dict:
+    got = np.asarray(got, dtype=np.int64)
+    mism = int((got != ref).sum())
+    assert mism == 0, f"{mism} int mismatches"
+    return {"mismatches": 0}
+
+
+def check(dtype_in: str, dtype_out: str, A_bits, B_bits, got, rows=None) -> dict:
+    """Compare a GPU result (numpy; bf16 output as uint16 bits) with the oracle
+    on the given rows of A (all rows when None)."""
+    ref = mm(A_bits, B_bits, dtype_in, rows=rows)
+    if dtype_in == "i8":
+        return check_exact(got, ref)
+    absab = mm(abs_bits(A_bits), abs_bits(B_bits), dtype_in, rows=rows)
+    if dtype_out == "bf16":
+        return check_bf16(got, ref, absab, K=np.asarray(A_bits).shape[1])
+    return check_float(got, ref, absab)

@@ -1,0 +1,67 @@
+// Device-side helpers shared by the tall-call and blocked-product kernels
+// (gfx950 / CDNA4 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "tcu.h"
+
+namespace tcu {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+
+// Input element size in bytes for a tcu_dtype.
+__host__ __device__ constexpr int in_bytes(int dt) { return dt == TCU_I8_I32 ? 1 : 2; }
+// Output element size in bytes for a tcu_dtype.
+__host__ __device__ constexpr int out_bytes(int dt) { return dt == TCU_BF16_BF16 ? 2 : 4; }
+
+template <typename T, typename S>
+__device__ __forceinline__ T bitcast(const S &s) {
+  static_assert(sizeof(T) == sizeof(S), "bitcast size");
+  return __builtin_bit_cast(T, s);
+}
+
+// ---------------------------------------------------------------- MFMA
+// One 16x16 output block of the unit: D = W * X + D, where the lane layout
+// of the 16-row operand W (here always the right matrix B, transposed: the
+// unit's resident "weights"), of the 16-column operand X (rows of the tall
+// left matrix) and of D is the CDNA matrix-core layout: lane l holds row
+// (l % 16) of W and column (l % 16) of X over a contiguous run of the
+// contracted index chosen by l / 16, and D rows 4*(l/16) .. 4*(l/16)+3 of
+// column (l % 16).  K is 32 (16-bit inputs) or 64 (int8) per instruction.
+__device__ __forceinline__ f32x4 mfma_k32(int dt, u32x4 w, u32x4 x, f32x4 d) {
+  if (dt == TCU_F16_F32)
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(bitcast<f16x8>(w), bitcast<f16x8>(x), d, 0, 0, 0);
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(bitcast<bf16x8>(w), bitcast<bf16x8>(x), d, 0, 0, 0);
+}
+
+__device__ __forceinline__ i32x4 mfma_i8_k64(u32x4 w, u32x4 x, i32x4 d) {
+  return __builtin_amdgcn_mfma_i32_16x16x64_i8(bitcast<i32x4>(w), bitcast<i32x4>(x), d, 0, 0, 0);
+}
+
+// Narrow forms: K = 16 for 16-bit inputs, K = 32 for int8 (8 bytes per lane).
+__device__ __forceinline__ f32x4 mfma_k16(int dt, u32x2 w, u32x2 x, f32x4 d) {
+  if (dt == TCU_F16_F32)
+    return __builtin_amdgcn_mfma_f32_16x16x16f16(bitcast<f16x4>(w), bitcast<f16x4>(x), d, 0, 0, 0);
+  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(bitcast<i16x4>(w), bitcast<i16x4>(x), d, 0, 0, 0);
+}
+
+__device__ __forceinline__ i32x4 mfma_i8_k32(u32x2 w, u32x2 x, i32x4 d) {
+  return __builtin_amdgcn_mfma_i32_16x16x32_i8(bitcast<long>(w), bitcast<long>(x), d, 0, 0, 0);
+}
+
+// binary32 -> bfloat16, round to nearest even (gfx950 v_cvt_pk_bf16_f32).
+__device__ __forceinline__ unsigned pack_bf16x2(float lo, float hi) {
+  __bf16 a = (__bf16)lo, b = (__bf16)hi;
+  return (unsigned)bitcast<unsigned short>(a) | ((unsigned)bitcast<unsigned short>(b) << 16);
+}
+
+}  // namespace tcu

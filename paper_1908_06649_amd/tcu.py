@@ -1,0 +1,203 @@
+"""Python binding of the C ABI in include/tcu.h (argument marshalling only).
+
+Functions carry the C names.  Matrices are torch tensors on the current HIP
+device; torch supplies device memory and the stream, nothing else -- every
+step of the computation runs in the library's HIP kernels.  There is no
+fallback: if ``libtcu.so`` is missing or fails to load, every call raises.
+
+    tcu_mm_tall(A, n, s, B, C)   C (n x s) = A (n x s) @ B (s x s)     (native call)
+    tcu_gemm(A, B, C, N)         C (N x N) = A @ B, unit size tcu_get_unit()
+
+The element types are taken from the tensors: (float16 -> float32),
+(bfloat16 -> float32), (bfloat16 -> bfloat16) or (int8 -> int32).  Calls are
+issued on torch's current stream and are asynchronous.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libtcu.so")
+
+TCU_OK = 0
+TCU_ERR_NULL = -1
+TCU_ERR_SHAPE = -2
+TCU_ERR_UNSUPPORTED = -3
+TCU_ERR_ALIGN = -4
+TCU_ERR_OVERLAP = -5
+TCU_ERR_HIP = -6
+TCU_ERR_NO_DEVICE = -7
+
+TCU_F16_F32 = 0
+TCU_BF16_F32 = 1
+TCU_BF16_BF16 = 2
+TCU_I8_I32 = 3
+
+# Every symbol include/tcu.h declares: name -> (restype, argtypes)
+_i64, _int, _vp = ctypes.c_int64, ctypes.c_int, ctypes.c_void_p
+SIGNATURES = {
+    "tcu_set_unit": (_int, [_int]),
+    "tcu_get_unit": (_int, []),
+    "tcu_set_dtype": (_int, [_int]),
+    "tcu_get_dtype": (_int, []),
+    "tcu_set_stream": (_int, [_vp]),
+    "tcu_get_stream": (_vp, []),
+    "tcu_mm_tall": (_int, [_vp, _i64, _int, _vp, _vp]),
+    "tcu_gemm": (_int, [_vp, _vp, _vp, _i64]),
+    "tcu_mm_tall_ex": (_int, [_vp, _i64, _int, _vp, _vp, _int, _vp]),
+    "tcu_gemm_ex": (_int, [_vp, _vp, _vp, _i64, _int, _int, _vp]),
+    "tcu_calls": (_i64, []),
+    "tcu_square_calls": (_i64, []),
+    "tcu_work": (_i64, []),
+    "tcu_reset_calls": (None, []),
+    "tcu_strerror": (ctypes.c_char_p, [_int]),
+}
+
+_lib = None
+
+
+class TcuError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {tcu_strerror(status)} (status {status})")
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded C library (raises if it was not built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(
+                f"{LIB_PATH} is missing: build the HIP library first "
+                "(python -c 'import __graft_entry__ as g; g.build()')")
+        handle = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            fn = getattr(handle, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = handle
+    return _lib
+
+
+def _check(rc: int, where: str) -> None:
+    if rc != TCU_OK:
+        raise TcuError(rc, where)
+
+
+def _dtype_code(a_dtype, c_dtype) -> int:
+    import torch
+    table = {
+        (torch.float16, torch.float32): TCU_F16_F32,
+        (torch.bfloat16, torch.float32): TCU_BF16_F32,
+        (torch.bfloat16, torch.bfloat16): TCU_BF16_BF16,
+        (torch.int8, torch.int32): TCU_I8_I32,
+    }
+    try:
+        return table[(a_dtype, c_dtype)]
+    except KeyError:
+        raise TcuError(TCU_ERR_UNSUPPORTED, f"dtype pair ({a_dtype}, {c_dtype})") from None
+
+
+def _marshal(where: str, tensors, numels):
+    """Check that tensors are contiguous, on one HIP device, and sized as the
+    call will read/write them; return their device pointers."""
+    dev = tensors[0].device
+    ptrs = []
+    for t, want in zip(tensors, numels):
+        if t.device != dev or t.device.type != "cuda":
+            raise ValueError(f"{where}: all matrices must be on the same HIP device")
+        if not t.is_contiguous():
+            raise ValueError(f"{where}: matrices must be contiguous (row-major)")
+        if t.numel() != want:
+            raise ValueError(f"{where}: expected {want} elements, got {t.numel()}")
+        ptrs.append(t.data_ptr())
+    return dev, ptrs
+
+
+def _stream_ptr(dev) -> int:
+    import torch
+    return torch.cuda.current_stream(dev).cuda_stream
+
+
+# ------------------------------------------------------------ configuration
+def tcu_set_unit(s: int) -> None:
+    _check(lib().tcu_set_unit(int(s)), "tcu_set_unit")
+
+
+def tcu_get_unit() -> int:
+    return int(lib().tcu_get_unit())
+
+
+def tcu_set_dtype(dtype: int) -> None:
+    _check(lib().tcu_set_dtype(int(dtype)), "tcu_set_dtype")
+
+
+def tcu_get_dtype() -> int:
+    return int(lib().tcu_get_dtype())
+
+
+def tcu_set_stream(stream_ptr: int | None) -> None:
+    _check(lib().tcu_set_stream(stream_ptr), "tcu_set_stream")
+
+
+def tcu_get_stream() -> int | None:
+    return lib().tcu_get_stream()
+
+
+# ------------------------------------------------------------------- calls
+def tcu_mm_tall(A, n: int, s: int, B, C) -> None:
+    """Native call: C (n x s) = A (n x s) @ B (s x s); s must equal the unit size."""
+    dt = _dtype_code(A.dtype, C.dtype)
+    dev, (pa, pb, pc) = _marshal("tcu_mm_tall", (A, B, C), (n * s, s * s, n * s))
+    L = lib()
+    _check(L.tcu_set_dtype(dt), "tcu_mm_tall")
+    _check(L.tcu_set_stream(_stream_ptr(dev)), "tcu_mm_tall")
+    _check(L.tcu_mm_tall(pa, int(n), int(s), pb, pc), "tcu_mm_tall")
+
+
+def tcu_gemm(A, B, C, N: int) -> None:
+    """Blocked product of Theorem 2: C (N x N) = A @ B with unit size tcu_get_unit()."""
+    dt = _dtype_code(A.dtype, C.dtype)
+    dev, (pa, pb, pc) = _marshal("tcu_gemm", (A, B, C), (N * N, N * N, N * N))
+    L = lib()
+    _check(L.tcu_set_dtype(dt), "tcu_gemm")
+    _check(L.tcu_set_stream(_stream_ptr(dev)), "tcu_gemm")
+    _check(L.tcu_gemm(pa, pb, pc, int(N)), "tcu_gemm")
+
+
+def tcu_mm_tall_ex(A, n: int, s: int, B, C, stream_ptr: int | None = None) -> None:
+    """Stateless native call (unit size, dtype and stream as arguments)."""
+    dt = _dtype_code(A.dtype, C.dtype)
+    dev, (pa, pb, pc) = _marshal("tcu_mm_tall_ex", (A, B, C), (n * s, s * s, n * s))
+    st = _stream_ptr(dev) if stream_ptr is None else stream_ptr
+    _check(lib().tcu_mm_tall_ex(pa, int(n), int(s), pb, pc, dt, st), "tcu_mm_tall_ex")
+
+
+def tcu_gemm_ex(A, B, C, N: int, s: int, stream_ptr: int | None = None) -> None:
+    """Stateless blocked product (unit size, dtype and stream as arguments)."""
+    dt = _dtype_code(A.dtype, C.dtype)
+    dev, (pa, pb, pc) = _marshal("tcu_gemm_ex", (A, B, C), (N * N, N * N, N * N))
+    st = _stream_ptr(dev) if stream_ptr is None else stream_ptr
+    _check(lib().tcu_gemm_ex(pa, pb, pc, int(N), int(s), dt, st), "tcu_gemm_ex")
+
+
+# --------------------------------------------------------- cost accounting
+def tcu_calls() -> int:
+    return int(lib().tcu_calls())
+
+
+def tcu_square_calls() -> int:
+    return int(lib().tcu_square_calls())
+
+
+def tcu_work() -> int:
+    return int(lib().tcu_work())
+
+
+def tcu_reset_calls() -> None:
+    lib().tcu_reset_calls()
+
+
+def tcu_strerror(status: int) -> str:
+    return lib().tcu_strerror(int(status)).decode()

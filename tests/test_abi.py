@@ -1,0 +1,187 @@
+"""C ABI tests that need no GPU: the library loads, exports every function
+include/tcu.h declares, and rejects bad arguments before any HIP call.
+
+Every call below with non-NULL fake pointers is built to fail validation, so
+no kernel can ever be launched on them.  The one call with valid arguments
+(expecting TCU_ERR_NO_DEVICE) runs only where no GPU is visible.
+"""
+import os
+import re
+import subprocess
+import threading
+
+import pytest
+import torch
+
+from paper_1908_06649_amd import tcu
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "tcu.h")
+
+# fake, 16-byte aligned, far-apart "device" addresses (never dereferenced)
+PA, PB, PC = 0x10000000, 0x20000000, 0x30000000
+
+
+@pytest.fixture(scope="module")
+def L():
+    lib = tcu.lib()
+    lib.tcu_set_unit(16)
+    lib.tcu_set_dtype(tcu.TCU_F16_F32)
+    lib.tcu_reset_calls()
+    return lib
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(tcu_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for must in ("tcu_mm_tall", "tcu_gemm", "tcu_set_unit", "tcu_set_dtype",
+                 "tcu_set_stream", "tcu_calls", "tcu_reset_calls", "tcu_strerror"):
+        assert must in names
+
+
+def test_library_exports_every_declared_symbol(L):
+    names = declared_functions()
+    assert set(names) == set(tcu.SIGNATURES), "binding and header disagree"
+    out = subprocess.run(["nm", "-D", "--defined-only", tcu.LIB_PATH],
+                         capture_output=True, text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (tcu_[a-z0-9_]+)$", out, flags=re.M))
+    assert set(names) <= exported
+    for n in names:
+        assert getattr(L, n) is not None
+
+
+def test_strerror_covers_all_codes(L):
+    for code in range(0, -8, -1):
+        msg = tcu.tcu_strerror(code)
+        assert msg and "unknown" not in msg
+    assert "unknown" in tcu.tcu_strerror(-99)
+
+
+def test_unit_and_dtype_config(L):
+    assert L.tcu_set_unit(32) == tcu.TCU_OK and L.tcu_get_unit() == 32
+    assert L.tcu_set_unit(8) == tcu.TCU_ERR_UNSUPPORTED and L.tcu_get_unit() == 32
+    assert L.tcu_set_unit(64) == tcu.TCU_ERR_UNSUPPORTED
+    assert L.tcu_set_unit(16) == tcu.TCU_OK
+    assert L.tcu_set_dtype(tcu.TCU_I8_I32) == tcu.TCU_OK and L.tcu_get_dtype() == tcu.TCU_I8_I32
+    assert L.tcu_set_dtype(4) == tcu.TCU_ERR_UNSUPPORTED and L.tcu_get_dtype() == tcu.TCU_I8_I32
+    assert L.tcu_set_dtype(-1) == tcu.TCU_ERR_UNSUPPORTED
+    assert L.tcu_set_dtype(tcu.TCU_F16_F32) == tcu.TCU_OK
+    assert L.tcu_set_stream(0x1234) == tcu.TCU_OK and L.tcu_get_stream() == 0x1234
+    assert L.tcu_set_stream(None) == tcu.TCU_OK and not L.tcu_get_stream()
+
+
+def test_config_is_per_thread(L):
+    L.tcu_set_unit(16)
+    seen = {}
+
+    def worker():
+        seen["before"] = L.tcu_get_unit()
+        L.tcu_set_unit(32)
+        seen["after"] = L.tcu_get_unit()
+
+    t = threading.Thread(target=worker)
+    t.start()
+    t.join()
+    assert seen == {"before": 16, "after": 32}
+    assert L.tcu_get_unit() == 16
+
+
+TALL_ERRORS = [
+    # (A, n, s, B, C, dtype) -> status
+    ((0, 4096, 16, PB, PC, 0), tcu.TCU_ERR_NULL),
+    ((PA, 4096, 16, 0, PC, 0), tcu.TCU_ERR_NULL),
+    ((PA, 4096, 16, PB, 0, 0), tcu.TCU_ERR_NULL),
+    ((PA, 4096, 8, PB, PC, 0), tcu.TCU_ERR_UNSUPPORTED),
+    ((PA, 4096, 24, PB, PC, 0), tcu.TCU_ERR_UNSUPPORTED),
+    ((PA, 4096, 16, PB, PC, 4), tcu.TCU_ERR_UNSUPPORTED),
+    ((PA, 4096, 16, PB, PC, -1), tcu.TCU_ERR_UNSUPPORTED),
+    ((PA, 15, 16, PB, PC, 0), tcu.TCU_ERR_SHAPE),          # n < s
+    ((PA, 31, 32, PB, PC, 1), tcu.TCU_ERR_SHAPE),
+    ((PA, 0, 16, PB, PC, 0), tcu.TCU_ERR_SHAPE),
+    ((PA, -5, 16, PB, PC, 0), tcu.TCU_ERR_SHAPE),
+    ((PA, (1 << 40) + 1, 16, PB, PC, 0), tcu.TCU_ERR_SHAPE),
+    ((PA + 8, 4096, 16, PB, PC, 0), tcu.TCU_ERR_ALIGN),
+    ((PA, 4096, 16, PB + 2, PC, 0), tcu.TCU_ERR_ALIGN),
+    ((PA, 4096, 16, PB, PC + 4, 0), tcu.TCU_ERR_ALIGN),
+    # C overlaps A: A spans 4096*16*2 bytes
+    ((PA, 4096, 16, PB, PA + 4096 * 16 * 2 - 16, 0), tcu.TCU_ERR_OVERLAP),
+    ((PA, 4096, 16, PB, PA - 4096 * 16 * 4 + 16, 0), tcu.TCU_ERR_OVERLAP),
+    # C overlaps B (B spans 16*16*2 bytes; C starts inside it)
+    ((PA, 4096, 16, PB, PB + 496, 0), tcu.TCU_ERR_OVERLAP),
+]
+
+
+@pytest.mark.parametrize("args,want", TALL_ERRORS)
+def test_tall_rejects(L, args, want):
+    L.tcu_reset_calls()
+    A, n, s, B, C, dt = args
+    assert L.tcu_mm_tall_ex(A, n, s, B, C, dt, None) == want
+    assert L.tcu_calls() == 0 and L.tcu_square_calls() == 0 and L.tcu_work() == 0
+
+
+def test_tall_stateful_checks_unit(L):
+    L.tcu_set_unit(16)
+    assert L.tcu_mm_tall(PA, 4096, 32, PB, PC) == tcu.TCU_ERR_UNSUPPORTED
+    assert L.tcu_mm_tall(0, 4096, 16, PB, PC) == tcu.TCU_ERR_NULL
+    assert L.tcu_mm_tall(PA, 8, 16, PB, PC) == tcu.TCU_ERR_SHAPE
+
+
+GEMM_ERRORS = [
+    # (A, B, C, N, s, dtype) -> status
+    ((0, PB, PC, 1024, 16, 0), tcu.TCU_ERR_NULL),
+    ((PA, 0, PC, 1024, 16, 0), tcu.TCU_ERR_NULL),
+    ((PA, PB, 0, 1024, 16, 0), tcu.TCU_ERR_NULL),
+    ((PA, PB, PC, 1024, 12, 0), tcu.TCU_ERR_UNSUPPORTED),
+    ((PA, PB, PC, 1024, 16, 9), tcu.TCU_ERR_UNSUPPORTED),
+    ((PA, PB, PC, 1000, 16, 0), tcu.TCU_ERR_SHAPE),          # N % s != 0
+    ((PA, PB, PC, 48, 32, 1), tcu.TCU_ERR_SHAPE),
+    ((PA, PB, PC, 16, 32, 1), tcu.TCU_ERR_SHAPE),            # N < s
+    ((PA, PB, PC, 0, 16, 0), tcu.TCU_ERR_SHAPE),
+    ((PA, PB, PC, (1 << 20) + 16, 16, 0), tcu.TCU_ERR_SHAPE),
+    ((PA, PB, PC, 1 << 17, 32, 3), tcu.TCU_ERR_SHAPE),       # int32 sums could overflow
+    ((PA + 4, PB, PC, 1024, 16, 0), tcu.TCU_ERR_ALIGN),
+    ((PA, PB, PC + 8, 1024, 16, 0), tcu.TCU_ERR_ALIGN),
+    ((PA, PB, PA + 1024 * 1024 * 2 - 16, 1024, 16, 0), tcu.TCU_ERR_OVERLAP),
+    ((PA, PB, PB, 1024, 16, 0), tcu.TCU_ERR_OVERLAP),
+]
+
+
+@pytest.mark.parametrize("args,want", GEMM_ERRORS)
+def test_gemm_rejects(L, args, want):
+    L.tcu_reset_calls()
+    A, B, C, N, s, dt = args
+    assert L.tcu_gemm_ex(A, B, C, N, s, dt, None) == want
+    assert L.tcu_calls() == 0
+
+
+def test_gemm_stateful_uses_unit(L):
+    L.tcu_set_unit(32)
+    L.tcu_set_dtype(tcu.TCU_BF16_F32)
+    assert L.tcu_gemm(PA, PB, PC, 48) == tcu.TCU_ERR_SHAPE     # 48 % 32 != 0
+    L.tcu_set_unit(16)
+    L.tcu_set_dtype(tcu.TCU_F16_F32)
+
+
+@pytest.mark.skipif(torch.cuda.device_count() > 0, reason="a HIP device is visible")
+def test_valid_arguments_without_device(L):
+    L.tcu_reset_calls()
+    assert L.tcu_mm_tall_ex(PA, 4096, 16, PB, PC, 0, None) == tcu.TCU_ERR_NO_DEVICE
+    assert L.tcu_gemm_ex(PA, PB, PC, 1024, 16, 0, None) == tcu.TCU_ERR_NO_DEVICE
+    # A and B may overlap (both are only read)
+    assert L.tcu_gemm_ex(PA, PA, PC, 1024, 16, 0, None) == tcu.TCU_ERR_NO_DEVICE
+    assert L.tcu_calls() == 0
+
+
+def test_python_binding_marshalling_errors():
+    A = torch.zeros(64, 16, dtype=torch.float16)
+    B = torch.zeros(16, 16, dtype=torch.float16)
+    C = torch.zeros(64, 16, dtype=torch.float32)
+    with pytest.raises(ValueError):          # host tensors are not device memory
+        tcu.tcu_mm_tall(A, 64, 16, B, C)
+    with pytest.raises(tcu.TcuError):        # unsupported dtype pair
+        tcu.tcu_mm_tall(A, 64, 16, B, C.to(torch.float16))
