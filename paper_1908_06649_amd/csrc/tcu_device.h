@@ -58,6 +58,31 @@ __device__ __forceinline__ i32x4 mfma_i8_k32(u32x2 w, u32x2 x, i32x4 d) {
   return __builtin_amdgcn_mfma_i32_16x16x32_i8(bitcast<long>(w), bitcast<long>(x), d, 0, 0, 0);
 }
 
+// ---------------------------------------------------------------- LDS
+#define TCU_LDS(T, p) ((__attribute__((address_space(3))) T *)(p))
+
+// Direct global -> LDS copy of 16 bytes per lane: lane l's bytes land at
+// lds_base + 16*l (lds_base must be wave-uniform).
+__device__ __forceinline__ void load_lds16(const void *gptr, void *lds_base) {
+  __builtin_amdgcn_global_load_lds(gptr, TCU_LDS(void, lds_base), 16, 0, 0);
+}
+
+// Transposing LDS reads (gfx950).  Within each group of 16 lanes, treat the
+// 8-byte segments the lanes point at as rows of a 16 x 4 (16-bit) or 16 x 8
+// (8-bit) matrix M.  ds_read_b64_tr_b16 returns to lane j the elements
+// M[4e + j/4][j%4], e = 0..3; ds_read_b64_tr_b8 returns M[2e + j/8][j%8],
+// e = 0..7.  So if lane s points at row k0 + s/4, columns c0 + 4(s%4) of a
+// row-major 16-bit matrix, lane j receives column c0 + j, rows k0 .. k0+3
+// (rows k0 .. k0+7 of column c0 + j for 8-bit, lane s pointing at row
+// k0 + s/2, columns c0 + 8(s%2)).
+__device__ __forceinline__ u32x2 lds_read_tr16(const void *p) {
+  return bitcast<u32x2>(__builtin_amdgcn_ds_read_tr16_b64_v4i16(TCU_LDS(i16x4, p)));
+}
+__device__ __forceinline__ u32x2 lds_read_tr8(const void *p) {
+  typedef int i32x2 __attribute__((ext_vector_type(2)));
+  return bitcast<u32x2>(__builtin_amdgcn_ds_read_tr8_b64_v2i32(TCU_LDS(i32x2, p)));
+}
+
 // binary32 -> bfloat16, round to nearest even (gfx950 v_cvt_pk_bf16_f32).
 __device__ __forceinline__ unsigned pack_bf16x2(float lo, float hi) {
   __bf16 a = (__bf16)lo, b = (__bf16)hi;

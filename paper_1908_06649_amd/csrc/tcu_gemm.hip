@@ -29,6 +29,9 @@
 // Workgroup order is XCD-aware: consecutive workgroup ids land on different
 // XCDs, so ids are remapped to give each XCD a contiguous, grouped range of
 // tiles that share A row-panels and B column-panels in its private L2.
+#include <cstdlib>
+#include <cstring>
+
 #include "tcu_device.h"
 #include "tcu_launch.h"
 
@@ -232,6 +235,215 @@ gemm_kernel(const unsigned char *__restrict__ A, const unsigned char *__restrict
   }
 }
 
+// ---------------------------------------------------------------------------
+// Full-tile kernel (N a multiple of 256): 256 x 256 output tile per
+// workgroup, 4 waves of 128 x 128, and a 4-deep ring of LDS stages, each
+// holding 64 bytes of the contracted index (32 16-bit or 64 int8 values,
+// i.e. one matrix-core K step, and one or two strips A_i of the unit).
+//   * Both operands go HBM/L2 -> LDS with direct 16-byte DMA loads
+//     (global_load_lds_dwordx4): no register staging, no VALU work.  Three
+//     stages are in flight while the fourth is consumed; each wave waits
+//     only for its own loads of the stage it is about to read (vmcnt), then
+//     a fence-free workgroup barrier makes every wave's part visible.
+//   * A stage of A is 256 rows x 64 bytes; lanes read their 16-byte
+//     fragment with ds_read_b128 (chunks XOR-swizzled by the row's position
+//     in its 16-row block: conflict-free, and the same per-lane offset
+//     serves every block, stage and K step through the immediate field).
+//   * A stage of B is kept row-major as it is in memory (k rows of 256
+//     columns); the weights operand (B^T) is formed by transposing LDS
+//     reads (ds_read_b64_tr_b16 / _tr_b8), chunks XOR-swizzled per row so
+//     the 16 lanes of a read group hit distinct banks.
+// ---------------------------------------------------------------------------
+constexpr int kFastKB = 64;                     // bytes of K per stage
+constexpr int kFastStage = 256 * kFastKB;       // 16 KiB per operand per stage
+constexpr int kFastRing = 4;                    // stages in the LDS ring
+
+// A stage: 64-byte rows (4 chunks); key: row position r in its 16-row block.
+__device__ __forceinline__ int fa_swz(int r) { return ((r >> 1) ^ (r >> 3)) & 3; }
+// B stage, 16-bit: 512-byte rows (32 chunks).
+__device__ __forceinline__ int fb16_swz(int k) { return ((k & 3) << 1) | (((k >> 3) & 3) << 3); }
+// B stage, int8: 256-byte rows (16 chunks).
+__device__ __forceinline__ int fb8_swz(int k) { return (k & 7) | (((k >> 4) & 1) << 3); }
+
+// Wait until at most n of this wave's DMA loads are in flight and all its
+// LDS reads have returned, then barrier without a memory fence.
+template <int n>
+__device__ __forceinline__ void ring_barrier() {
+  __builtin_amdgcn_s_waitcnt((n & 15) | (7 << 4) | (0 << 8) | (((n >> 4) & 3) << 14));
+  __builtin_amdgcn_s_barrier();
+}
+
+template <int DT>
+__global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(1, 1))) void
+gemm_fast_kernel(const unsigned char *__restrict__ A, const unsigned char *__restrict__ B,
+                 unsigned char *__restrict__ C, int N, int tiles_m, int tiles_n) {
+  constexpr bool kI8 = (DT == TCU_I8_I32);
+  constexpr int ES = in_bytes(DT);
+  constexpr int KE = kFastKB / ES;     // contracted elements per stage
+  constexpr int BROW = 256 * ES;       // bytes per B row in a stage
+  constexpr int FM = 8, FN = 8;        // 16 x 16 blocks per wave (128 x 128)
+  constexpr int kLoadsPerStage = 8;    // DMA instructions per wave per stage
+  typedef typename std::conditional<kI8, i32x4, f32x4>::type Acc;
+
+  // One __shared__ object per ring slot: distinct objects let the compiler
+  // see that the refill of one slot never aliases reads of another.
+  __shared__ __attribute__((aligned(1024))) unsigned char sA0[kFastStage], sA1[kFastStage],
+      sA2[kFastStage], sA3[kFastStage];
+  __shared__ __attribute__((aligned(1024))) unsigned char sB0[kFastStage], sB1[kFastStage],
+      sB2[kFastStage], sB3[kFastStage];
+  auto slotA = [&](int s) -> unsigned char * { return s == 0 ? sA0 : s == 1 ? sA1 : s == 2 ? sA2 : sA3; };
+  auto slotB = [&](int s) -> unsigned char * { return s == 0 ? sB0 : s == 1 ? sB1 : s == 2 ? sB2 : sB3; };
+
+  int tm, tn;
+  map_tile(blockIdx.x, tiles_m, tiles_n, tm, tn);
+  const int m0 = tm * 256, n0 = tn * 256;
+  const int64_t ld = (int64_t)N * ES;
+  const int lane = threadIdx.x & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int r = lane & 15, g = lane >> 4;
+  const int wm = wid >> 1, wn = wid & 1;
+  const int nk = N / KE;
+
+  // DMA sources of this wave (for K stage 0).  A: 16-row blocks 4w..4w+3,
+  // lane -> (row l/4 of the block, physical chunk l%4).  B: 1 KiB blocks
+  // 4w..4w+3 (2 rows of 512 B, or 4 rows of 256 B).
+  const unsigned char *a_src[4], *b_src[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int rb = lane >> 2;
+    const int row = (wid * 4 + i) * 16 + rb;
+    a_src[i] = A + (int64_t)(m0 + row) * ld + 16 * ((lane & 3) ^ fa_swz(rb));
+    const int blk = wid * 4 + i;
+    int krow, c;
+    if constexpr (!kI8) {
+      krow = blk * 2 + (lane >> 5);
+      c = (lane & 31) ^ fb16_swz(krow);
+    } else {
+      krow = blk * 4 + (lane >> 4);
+      c = (lane & 15) ^ fb8_swz(krow);
+    }
+    b_src[i] = B + (int64_t)krow * ld + (int64_t)n0 * ES + 16 * c;
+  }
+  const int64_t b_step = (int64_t)KE * ld;   // bytes between K stages of B
+
+  auto issue = [&](int slot, int t) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      load_lds16(a_src[i] + (int64_t)t * kFastKB, slotA(slot) + (wid * 4 + i) * 1024);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      load_lds16(b_src[i] + (int64_t)t * b_step, slotB(slot) + (wid * 4 + i) * 1024);
+  };
+
+  // Per-lane LDS read offsets (stage 0, block 0); blocks, stages and the
+  // second transposed read are immediate offsets from these.
+  const int x_off = (wm * 128 + r) * kFastKB + 16 * (g ^ fa_swz(r));
+  int w_off[FN];
+#pragma unroll
+  for (int fn = 0; fn < FN; ++fn) {
+    const int nbase = wn * 128 + fn * 16;
+    if constexpr (!kI8) {
+      const int n = nbase + 4 * (r & 3);
+      const int k0 = 8 * g + (r >> 2);
+      w_off[fn] = k0 * BROW + 16 * ((n >> 3) ^ fb16_swz(k0)) + ((2 * n) & 15);
+    } else {
+      const int n = nbase + 8 * (r & 1);
+      const int k0 = 16 * g + (r >> 1);
+      w_off[fn] = k0 * BROW + 16 * ((n >> 4) ^ fb8_swz(k0)) + (n & 15);
+    }
+  }
+  constexpr int kW1 = (kI8 ? 8 : 4) * BROW;   // second transposed read: +4 / +8 rows
+
+  Acc acc[FN][FM];
+#pragma unroll
+  for (int a = 0; a < FN; ++a)
+#pragma unroll
+    for (int b = 0; b < FM; ++b) acc[a][b] = Acc{0, 0, 0, 0};
+
+  // Matrix-core work of one K stage in ring slot `slot`: the calls
+  // A_i[rows] * B_{i,j} of this K step for the wave's 8 x 8 blocks.
+  auto compute = [&](int slot) {
+    const unsigned char *sa = slotA(slot);
+    const unsigned char *sb = slotB(slot);
+    u32x4 xf[FM];
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm) xf[fm] = *(const u32x4 *)(sa + x_off + fm * 16 * kFastKB);
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn) {
+      u32x2 w0, w1;
+      if constexpr (!kI8) {
+        w0 = lds_read_tr16(sb + w_off[fn]);
+        w1 = lds_read_tr16(sb + w_off[fn] + kW1);
+      } else {
+        w0 = lds_read_tr8(sb + w_off[fn]);
+        w1 = lds_read_tr8(sb + w_off[fn] + kW1);
+      }
+      const u32x4 wf = {w0[0], w0[1], w1[0], w1[1]};
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm) {
+        if constexpr (kI8)
+          acc[fn][fm] = mfma_i8_k64(wf, xf[fm], acc[fn][fm]);
+        else
+          acc[fn][fm] = mfma_k32(DT, wf, xf[fm], acc[fn][fm]);
+      }
+    }
+  };
+
+  // One K step from ring slot S (= t mod 4): wait until this wave's loads
+  // of the step are done (kWait later loads may stay in flight), barrier
+  // (every wave's part is visible, and every wave is done with the slot of
+  // step t-1), refill that slot with step t+3 if kRefill, compute.
+  auto step = [&](auto S, auto kWait, auto kRefill, int t) {
+    constexpr int s = decltype(S)::value;
+    ring_barrier<decltype(kWait)::value>();
+    if constexpr (decltype(kRefill)::value) issue((s + 3) & 3, t + 3);
+    compute(s);
+  };
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  using I3 = std::integral_constant<int, 3>;
+  using W2 = std::integral_constant<int, 2 * kLoadsPerStage>;
+  using W1 = std::integral_constant<int, kLoadsPerStage>;
+  using W0 = std::integral_constant<int, 0>;
+  using Yes = std::true_type;
+  using No = std::false_type;
+
+  // nk is a multiple of 4 here (N % 256 == 0).  Steady state: branch-free.
+  issue(0, 0);
+  issue(1, 1);
+  issue(2, 2);
+  int t = 0;
+  for (; t < nk - 4; t += 4) {
+    step(I0{}, W2{}, Yes{}, t);
+    step(I1{}, W2{}, Yes{}, t + 1);
+    step(I2{}, W2{}, Yes{}, t + 2);
+    step(I3{}, W2{}, Yes{}, t + 3);
+  }
+  // Last four steps: stage nk-1 is the final refill.
+  step(I0{}, W2{}, Yes{}, t);
+  step(I1{}, W2{}, No{}, t + 1);
+  step(I2{}, W1{}, No{}, t + 2);
+  step(I3{}, W0{}, No{}, t + 3);
+
+  // Epilogue: lane holds C[row][col .. col+3] of every accumulator block.
+#pragma unroll
+  for (int fn = 0; fn < FN; ++fn) {
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm) {
+      const int row = m0 + wm * 128 + fm * 16 + r;
+      const int col = n0 + wn * 128 + fn * 16 + 4 * g;
+      if constexpr (DT == TCU_BF16_BF16) {
+        const f32x4 v = acc[fn][fm];
+        *(u32x2 *)(C + ((int64_t)row * N + col) * 2) =
+            u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+      } else {
+        *(u32x4 *)(C + ((int64_t)row * N + col) * 4) = bitcast<u32x4>(acc[fn][fm]);
+      }
+    }
+  }
+}
+
 template <int DT, int BM, int BN, int WM, int WN>
 hipError_t launch_cfg(const void *A, const void *B, void *C, int64_t N, hipStream_t stream) {
   const int tiles_m = (int)((N + BM - 1) / BM), tiles_n = (int)((N + BN - 1) / BN);
@@ -241,11 +453,32 @@ hipError_t launch_cfg(const void *A, const void *B, void *C, int64_t N, hipStrea
   return hipGetLastError();
 }
 
+// Kernel selection: TCU_GEMM_KERNEL=fast forces the full-tile kernel
+// wherever N % 256 == 0, =general forces the general kernel; unset or
+// =auto picks by size.
+enum class GemmPath { kAuto, kFast, kGeneral };
+GemmPath gemm_path() {
+  const char *v = std::getenv("TCU_GEMM_KERNEL");
+  if (!v) return GemmPath::kAuto;
+  if (!std::strcmp(v, "fast")) return GemmPath::kFast;
+  if (!std::strcmp(v, "general")) return GemmPath::kGeneral;
+  return GemmPath::kAuto;
+}
+
 template <int DT>
 hipError_t launch_dt(const void *A, const void *B, void *C, int64_t N, hipStream_t stream,
                      int num_cus) {
   // Big tiles when they fill the chip; otherwise smaller tiles for more workgroups.
   const int64_t big_tiles = ((N + 255) / 256) * ((N + 255) / 256);
+  const GemmPath path = gemm_path();
+  const bool fast_ok = (N % 256 == 0);
+  if (fast_ok && (path == GemmPath::kFast || (path == GemmPath::kAuto && big_tiles >= num_cus))) {
+    const int t = (int)(N / 256);
+    hipLaunchKernelGGL((gemm_fast_kernel<DT>), dim3(t * t), dim3(256), 0, stream,
+                       (const unsigned char *)A, (const unsigned char *)B, (unsigned char *)C,
+                       (int)N, t, t);
+    return hipGetLastError();
+  }
   if (big_tiles >= num_cus) return launch_cfg<DT, 256, 256, 2, 2>(A, B, C, N, stream);
   return launch_cfg<DT, 128, 128, 2, 2>(A, B, C, N, stream);
 }

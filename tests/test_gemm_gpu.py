@@ -123,3 +123,45 @@ def test_workload_i8_N8192_s32_sampled():
     got = run_gemm(A, B, 32, "i32")
     rows = _sample_rows(8192, 24, 2)
     compare.check("i8", "i32", inputs.bits(A), inputs.bits(B), got[rows], rows=rows)
+
+
+# Both kernels of the product on sizes where either applies (N % 256 == 0):
+# the full-tile kernel (DMA-fed LDS ring, transposing reads) and the general
+# one (register-staged, predicated tails).
+@pytest.mark.parametrize("path", ["fast", "general"])
+@pytest.mark.parametrize("din,dout", DTYPES)
+@pytest.mark.parametrize("N,s", [(256, 16), (512, 32), (1280, 32)])
+def test_kernel_paths(monkeypatch, path, din, dout, N, s):
+    monkeypatch.setenv("TCU_GEMM_KERNEL", path)
+    A, B = draw_pair((N, N), (N, N), din, seed=N + 3 * s)
+    got = run_gemm(A, B, s, dout)
+    compare.check(din, dout, inputs.bits(A), inputs.bits(B), got)
+
+
+@pytest.mark.parametrize("path", ["fast", "general"])
+@pytest.mark.parametrize("din,dout", DTYPES)
+def test_kernel_paths_identity_permutation(monkeypatch, path, din, dout):
+    monkeypatch.setenv("TCU_GEMM_KERNEL", path)
+    N, s = 768, 16
+    A, _ = draw_pair((N, N), (N, N), din, seed=11)
+    got = run_gemm(A, inputs.identity(N, din), s, dout)
+    assert np.array_equal(got, to_np(A.to(inputs.TORCH_DTYPE[dout])))
+    P, perm = inputs.permutation(N, din, 12)
+    got = run_gemm(A, P, s, dout)
+    assert np.array_equal(got, to_np(A[:, perm].to(inputs.TORCH_DTYPE[dout])))
+
+
+@pytest.mark.parametrize("path", ["fast", "general"])
+def test_kernel_paths_composition(monkeypatch, path):
+    monkeypatch.setenv("TCU_GEMM_KERNEL", path)
+    N, s = 256, 32
+    A, B = draw_pair((N, N), (N, N), "i8", seed=13)
+    full = run_gemm(A, B, s, "i32").astype(np.int64)
+    q = N // s
+    acc = np.zeros((N, N), dtype=np.int64)
+    for i in range(q):
+        Ai = A[:, i * s:(i + 1) * s].contiguous()
+        for j in range(q):
+            Bij = B[i * s:(i + 1) * s, j * s:(j + 1) * s].contiguous()
+            acc[:, j * s:(j + 1) * s] += run_tall(Ai, Bij, s, "i32").astype(np.int64)
+    assert np.array_equal(full, acc)
