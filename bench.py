@@ -203,17 +203,22 @@ def cpu_baseline(w: "Workload", target_s: float = 15.0) -> dict:
     N, dt = sp["N"], sp["dtype"]
     Ab, Bb = inputs.bits(w.A), inputs.bits(w.B)
     rng = np.random.default_rng(123)
-    probe = np.sort(rng.choice(N, 4, replace=False))
-    t0 = time.perf_counter()
-    oracle.mm(Ab, Bb, dt, rows=probe)
-    per_row = (time.perf_counter() - t0) / len(probe)
-    R = int(max(8, min(N, target_s / max(per_row, 1e-9))))
+    # two probes separate the per-call setup (decoding B) from the per-row cost
+    t_probe = []
+    for k in (8, 40):
+        rows_p = np.sort(rng.choice(N, k, replace=False))
+        t0 = time.perf_counter()
+        oracle.mm(Ab, Bb, dt, rows=rows_p)
+        t_probe.append(time.perf_counter() - t0)
+    per_row = max((t_probe[1] - t_probe[0]) / 32, 1e-9)
+    fixed = max(t_probe[0] - 8 * per_row, 0.0)
+    R = int(max(8, min(N, (target_s - fixed) / per_row)))
     rows = np.sort(rng.choice(N, R, replace=False))
     t0 = time.perf_counter()
     ref = oracle.mm(Ab, Bb, dt, rows=rows)
     secs = time.perf_counter() - t0
     got = w.C[rows].cpu()
-    got = got.view(np.int16) if False else got.numpy()
+    got = got.numpy()
     if dt == "i8":
         parity = compare.check_exact(got, ref)
     else:

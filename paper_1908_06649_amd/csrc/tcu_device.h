@@ -43,6 +43,22 @@ __device__ __forceinline__ f32x4 mfma_k32(int dt, u32x4 w, u32x4 x, f32x4 d) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(bitcast<bf16x8>(w), bitcast<bf16x8>(x), d, 0, 0, 0);
 }
 
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef int i32x16 __attribute__((ext_vector_type(16)));
+
+// 32 x 32 output blocks: K = 16 (16-bit inputs) or 32 (int8) per
+// instruction, 16 bytes of operand per lane.  Lane l holds row (l % 32) of
+// W and column (l % 32) of X over the contracted run selected by l / 32,
+// and D rows 8*(j/4) + 4*(l/32) + (j%4), j = 0..15, of column (l % 32).
+__device__ __forceinline__ f32x16 mfma32_k16(int dt, u32x4 w, u32x4 x, f32x16 d) {
+  if (dt == TCU_F16_F32)
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(bitcast<f16x8>(w), bitcast<f16x8>(x), d, 0, 0, 0);
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(bitcast<bf16x8>(w), bitcast<bf16x8>(x), d, 0, 0, 0);
+}
+__device__ __forceinline__ i32x16 mfma32_i8_k32(u32x4 w, u32x4 x, i32x16 d) {
+  return __builtin_amdgcn_mfma_i32_32x32x32_i8(bitcast<i32x4>(w), bitcast<i32x4>(x), d, 0, 0, 0);
+}
+
 __device__ __forceinline__ i32x4 mfma_i8_k64(u32x4 w, u32x4 x, i32x4 d) {
   return __builtin_amdgcn_mfma_i32_16x16x64_i8(bitcast<i32x4>(w), bitcast<i32x4>(x), d, 0, 0, 0);
 }
@@ -65,6 +81,31 @@ __device__ __forceinline__ i32x4 mfma_i8_k32(u32x2 w, u32x2 x, i32x4 d) {
 // lds_base + 16*l (lds_base must be wave-uniform).
 __device__ __forceinline__ void load_lds16(const void *gptr, void *lds_base) {
   __builtin_amdgcn_global_load_lds(gptr, TCU_LDS(void, lds_base), 16, 0, 0);
+}
+
+// LDS byte address of a __shared__ object.
+__device__ __forceinline__ unsigned lds_addr(const void *p) {
+  return (unsigned)(uintptr_t)(const __attribute__((address_space(3))) char *)p;
+}
+
+// The same direct copy issued as an instruction the compiler cannot see
+// into: it then inserts no waits of its own for it, so a multi-stage ring in
+// one LDS array keeps its later stages in flight.  The caller orders it with
+// explicit vmcnt waits and barriers.  lds_base: wave-uniform LDS address.
+__device__ __forceinline__ void dma_lds16(const void *gptr, unsigned lds_base) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(gptr), "s"(lds_base)
+               : "memory", "m0");
+}
+
+// The same with a wave-uniform 64-bit base and a per-lane 32-bit offset.
+__device__ __forceinline__ void dma_lds16_saddr(const void *gbase, unsigned voff,
+                                                unsigned lds_base) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(voff), "s"(gbase), "s"(lds_base)
+               : "memory", "m0");
 }
 
 // Transposing LDS reads (gfx950).  Within each group of 16 lanes, treat the

@@ -38,6 +38,16 @@
 namespace tcu {
 namespace {
 
+#ifndef TCU_GROUP_M
+#define TCU_GROUP_M 8
+#endif
+#ifndef TCU_XCD_REMAP
+#define TCU_XCD_REMAP 1
+#endif
+#ifndef TCU_RING
+#define TCU_RING 5
+#endif
+
 constexpr int kBKB = 128;  // bytes of the contracted index per K-step and LDS row
 
 __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row ^ (row >> 3)) & 7); }
@@ -46,8 +56,8 @@ __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row ^ 
 __device__ __forceinline__ void map_tile(int pid, int tiles_m, int tiles_n, int &tm, int &tn) {
   const int total = tiles_m * tiles_n;
   constexpr int kXcds = 8;
-  if (total % kXcds == 0) pid = (pid % kXcds) * (total / kXcds) + pid / kXcds;
-  constexpr int kGroupM = 8;
+  if (TCU_XCD_REMAP && total % kXcds == 0) pid = (pid % kXcds) * (total / kXcds) + pid / kXcds;
+  constexpr int kGroupM = TCU_GROUP_M;
   const int per_group = kGroupM * tiles_n;
   const int group = pid / per_group;
   const int first_m = group * kGroupM;
@@ -237,62 +247,70 @@ gemm_kernel(const unsigned char *__restrict__ A, const unsigned char *__restrict
 
 // ---------------------------------------------------------------------------
 // Full-tile kernel (N a multiple of 256): 256 x 256 output tile per
-// workgroup, 4 waves of 128 x 128, and a 4-deep ring of LDS stages, each
-// holding 64 bytes of the contracted index (32 16-bit or 64 int8 values,
-// i.e. one matrix-core K step, and one or two strips A_i of the unit).
+// workgroup and a ring of LDS stages, each holding 64 bytes of the
+// contracted index (32 16-bit or 64 int8 values: one matrix-core K step, and
+// one or two strips A_i of the unit).
 //   * Both operands go HBM/L2 -> LDS with direct 16-byte DMA loads
-//     (global_load_lds_dwordx4): no register staging, no VALU work.  Three
-//     stages are in flight while the fourth is consumed; each wave waits
-//     only for its own loads of the stage it is about to read (vmcnt), then
-//     a fence-free workgroup barrier makes every wave's part visible.
-//   * A stage of A is 256 rows x 64 bytes; lanes read their 16-byte
-//     fragment with ds_read_b128 (chunks XOR-swizzled by the row's position
-//     in its 16-row block: conflict-free, and the same per-lane offset
-//     serves every block, stage and K step through the immediate field).
+//     (global_load_lds_dwordx4): no register staging, no VALU work.
+//   * A stage of A is 256 rows x 64 bytes, kept as 1 KiB blocks of 16 rows
+//     stored chunk-major (the DMA lane -> row/chunk assignment does this for
+//     free), so every fragment read is a linear ds_read_b128, the access
+//     pattern LDS serves at full rate.
 //   * A stage of B is kept row-major as it is in memory (k rows of 256
 //     columns); the weights operand (B^T) is formed by transposing LDS
 //     reads (ds_read_b64_tr_b16 / _tr_b8), chunks XOR-swizzled per row so
 //     the 16 lanes of a read group hit distinct banks.
+//   * The DMA is issued through an instruction the compiler cannot see
+//     into, so it adds no conservative waits; the kernel orders it with
+//     explicit vmcnt waits and fence-free barriers.
 // ---------------------------------------------------------------------------
 constexpr int kFastKB = 64;                     // bytes of K per stage
 constexpr int kFastStage = 256 * kFastKB;       // 16 KiB per operand per stage
-constexpr int kFastRing = 4;                    // stages in the LDS ring
 
-// A stage: 64-byte rows (4 chunks); key: row position r in its 16-row block.
-__device__ __forceinline__ int fa_swz(int r) { return ((r >> 1) ^ (r >> 3)) & 3; }
 // B stage, 16-bit: 512-byte rows (32 chunks).
 __device__ __forceinline__ int fb16_swz(int k) { return ((k & 3) << 1) | (((k >> 3) & 3) << 3); }
 // B stage, int8: 256-byte rows (16 chunks).
 __device__ __forceinline__ int fb8_swz(int k) { return (k & 7) | (((k >> 4) & 1) << 3); }
 
-// Wait until at most n of this wave's DMA loads are in flight and all its
-// LDS reads have returned, then barrier without a memory fence.
+// ---------------------------------------------------------------------------
+// The full-tile kernel runs 8 waves, two per SIMD, in two groups.  Group 0 (waves 0-3) owns rows 0-127 of the 256 x 256 tile, group 1
+// (waves 4-7) rows 128-255; wave q of a group owns columns 64q .. 64q+63.
+// Each K stage is two phases separated by barriers:
+//   phase A(t): group 0 runs its matrix-core work of stage t while group 1
+//               issues DMA loads and reads its fragments of stage t;
+//   phase B(t): group 1 runs its matrix-core work of stage t while group 0
+//               issues DMA loads and reads its fragments of stage t+1.
+// A wave stalled on memory (full load queues, late data) therefore never
+// idles its SIMD's matrix core: the other wave on that SIMD is computing,
+// with raised issue priority.  Group 0 loads the A part of every stage and
+// group 1 the B part (4 DMA instructions per wave per stage).
+// Ring bookkeeping: the slot of stage t has been read by group 0 (in
+// B(t-1)) and by group 1 (in A(t)) once A(t) ends, so it is refilled with
+// stage t+kRing in B(t) (A part, group 0) and A(t+1) (B part, group 1).
+// Stage t+1 must be complete when A(t) ends, so every wave waits there for
+// its own loads of stage t+1 before the barrier.
+// ---------------------------------------------------------------------------
 template <int n>
-__device__ __forceinline__ void ring_barrier() {
+__device__ __forceinline__ void vm_wait_barrier() {
   __builtin_amdgcn_s_waitcnt((n & 15) | (7 << 4) | (0 << 8) | (((n >> 4) & 3) << 14));
   __builtin_amdgcn_s_barrier();
 }
 
-template <int DT>
-__global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(1, 1))) void
-gemm_fast_kernel(const unsigned char *__restrict__ A, const unsigned char *__restrict__ B,
-                 unsigned char *__restrict__ C, int N, int tiles_m, int tiles_n) {
+template <int DT, int kRing>
+__global__ __attribute__((amdgpu_flat_work_group_size(512, 512), amdgpu_waves_per_eu(2, 2))) void
+gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restrict__ B,
+               unsigned char *__restrict__ C, int N, int tiles_m, int tiles_n) {
   constexpr bool kI8 = (DT == TCU_I8_I32);
   constexpr int ES = in_bytes(DT);
   constexpr int KE = kFastKB / ES;     // contracted elements per stage
   constexpr int BROW = 256 * ES;       // bytes per B row in a stage
-  constexpr int FM = 8, FN = 8;        // 16 x 16 blocks per wave (128 x 128)
-  constexpr int kLoadsPerStage = 8;    // DMA instructions per wave per stage
+  constexpr int FM = 8, FN = 4;        // 16 x 16 blocks per wave (128 x 64)
+  constexpr int kDma = 4;              // DMA instructions per wave per stage
+  static_assert(kRing - 2 <= 3, "waits cover at most 3 later stages");
   typedef typename std::conditional<kI8, i32x4, f32x4>::type Acc;
 
-  // One __shared__ object per ring slot: distinct objects let the compiler
-  // see that the refill of one slot never aliases reads of another.
-  __shared__ __attribute__((aligned(1024))) unsigned char sA0[kFastStage], sA1[kFastStage],
-      sA2[kFastStage], sA3[kFastStage];
-  __shared__ __attribute__((aligned(1024))) unsigned char sB0[kFastStage], sB1[kFastStage],
-      sB2[kFastStage], sB3[kFastStage];
-  auto slotA = [&](int s) -> unsigned char * { return s == 0 ? sA0 : s == 1 ? sA1 : s == 2 ? sA2 : sA3; };
-  auto slotB = [&](int s) -> unsigned char * { return s == 0 ? sB0 : s == 1 ? sB1 : s == 2 ? sB2 : sB3; };
+  __shared__ __attribute__((aligned(1024))) unsigned char sA[kRing * kFastStage];
+  __shared__ __attribute__((aligned(1024))) unsigned char sB[kRing * kFastStage];
 
   int tm, tn;
   map_tile(blockIdx.x, tiles_m, tiles_n, tm, tn);
@@ -300,48 +318,46 @@ gemm_fast_kernel(const unsigned char *__restrict__ A, const unsigned char *__res
   const int64_t ld = (int64_t)N * ES;
   const int lane = threadIdx.x & 63;
   const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int grp = wid >> 2, q = wid & 3;
   const int r = lane & 15, g = lane >> 4;
-  const int wm = wid >> 1, wn = wid & 1;
   const int nk = N / KE;
 
-  // DMA sources of this wave (for K stage 0).  A: 16-row blocks 4w..4w+3,
-  // lane -> (row l/4 of the block, physical chunk l%4).  B: 1 KiB blocks
-  // 4w..4w+3 (2 rows of 512 B, or 4 rows of 256 B).
-  const unsigned char *a_src[4], *b_src[4];
+  // This wave's DMA share of a stage: group 0 -> A blocks 4q..4q+3 (16 rows
+  // each, stored chunk-major), group 1 -> B blocks 4q..4q+3 (1 KiB each).
+  // Wave-uniform 64-bit base + per-lane 32-bit offsets (saddr form).
+  const unsigned char *gbase = grp == 0 ? A + (int64_t)m0 * ld : B + (int64_t)n0 * ES;
+  const int64_t gstep = grp == 0 ? (int64_t)kFastKB : (int64_t)KE * ld;
+  unsigned voff[kDma];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int rb = lane >> 2;
-    const int row = (wid * 4 + i) * 16 + rb;
-    a_src[i] = A + (int64_t)(m0 + row) * ld + 16 * ((lane & 3) ^ fa_swz(rb));
-    const int blk = wid * 4 + i;
-    int krow, c;
-    if constexpr (!kI8) {
-      krow = blk * 2 + (lane >> 5);
-      c = (lane & 31) ^ fb16_swz(krow);
+  for (int i = 0; i < kDma; ++i) {
+    const int blk = q * 4 + i;
+    if (grp == 0) {
+      voff[i] = (unsigned)((blk * 16 + (lane & 15)) * ld) + 16u * (lane >> 4);
     } else {
-      krow = blk * 4 + (lane >> 4);
-      c = (lane & 15) ^ fb8_swz(krow);
+      int krow, c;
+      if constexpr (!kI8) {
+        krow = blk * 2 + (lane >> 5);
+        c = (lane & 31) ^ fb16_swz(krow);
+      } else {
+        krow = blk * 4 + (lane >> 4);
+        c = (lane & 15) ^ fb8_swz(krow);
+      }
+      voff[i] = (unsigned)(krow * ld) + 16u * c;
     }
-    b_src[i] = B + (int64_t)krow * ld + (int64_t)n0 * ES + 16 * c;
   }
-  const int64_t b_step = (int64_t)KE * ld;   // bytes between K stages of B
-
-  auto issue = [&](int slot, int t) {
+  const unsigned lds0 = (grp == 0 ? lds_addr(sA) : lds_addr(sB)) + q * 4 * 1024;
+  auto issue = [&](int slot_, int t) {
+    const unsigned char *base = gbase + (int64_t)t * gstep;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      load_lds16(a_src[i] + (int64_t)t * kFastKB, slotA(slot) + (wid * 4 + i) * 1024);
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      load_lds16(b_src[i] + (int64_t)t * b_step, slotB(slot) + (wid * 4 + i) * 1024);
+    for (int i = 0; i < kDma; ++i) dma_lds16_saddr(base, voff[i], lds0 + slot_ * kFastStage + i * 1024);
   };
 
-  // Per-lane LDS read offsets (stage 0, block 0); blocks, stages and the
-  // second transposed read are immediate offsets from these.
-  const int x_off = (wm * 128 + r) * kFastKB + 16 * (g ^ fa_swz(r));
+  // Fragment offsets (stage 0): rows 128*grp.. of A, columns 64q.. of B^T.
+  const int x_off = grp * 8 * 1024 + 16 * lane;
   int w_off[FN];
 #pragma unroll
   for (int fn = 0; fn < FN; ++fn) {
-    const int nbase = wn * 128 + fn * 16;
+    const int nbase = q * 64 + fn * 16;
     if constexpr (!kI8) {
       const int n = nbase + 4 * (r & 3);
       const int k0 = 8 * g + (r >> 2);
@@ -352,7 +368,7 @@ gemm_fast_kernel(const unsigned char *__restrict__ A, const unsigned char *__res
       w_off[fn] = k0 * BROW + 16 * ((n >> 4) ^ fb8_swz(k0)) + (n & 15);
     }
   }
-  constexpr int kW1 = (kI8 ? 8 : 4) * BROW;   // second transposed read: +4 / +8 rows
+  constexpr int kW1 = (kI8 ? 8 : 4) * BROW;
 
   Acc acc[FN][FM];
 #pragma unroll
@@ -360,14 +376,12 @@ gemm_fast_kernel(const unsigned char *__restrict__ A, const unsigned char *__res
 #pragma unroll
     for (int b = 0; b < FM; ++b) acc[a][b] = Acc{0, 0, 0, 0};
 
-  // Matrix-core work of one K stage in ring slot `slot`: the calls
-  // A_i[rows] * B_{i,j} of this K step for the wave's 8 x 8 blocks.
-  auto compute = [&](int slot) {
-    const unsigned char *sa = slotA(slot);
-    const unsigned char *sb = slotB(slot);
-    u32x4 xf[FM];
+  u32x4 xf[FM], wf[FN];
+  auto read_frags = [&](int slot_) {
+    const unsigned char *sa = sA + slot_ * kFastStage;
+    const unsigned char *sb = sB + slot_ * kFastStage;
 #pragma unroll
-    for (int fm = 0; fm < FM; ++fm) xf[fm] = *(const u32x4 *)(sa + x_off + fm * 16 * kFastKB);
+    for (int fm = 0; fm < FM; ++fm) xf[fm] = *(const u32x4 *)(sa + x_off + fm * 1024);
 #pragma unroll
     for (int fn = 0; fn < FN; ++fn) {
       u32x2 w0, w1;
@@ -378,61 +392,74 @@ gemm_fast_kernel(const unsigned char *__restrict__ A, const unsigned char *__res
         w0 = lds_read_tr8(sb + w_off[fn]);
         w1 = lds_read_tr8(sb + w_off[fn] + kW1);
       }
-      const u32x4 wf = {w0[0], w0[1], w1[0], w1[1]};
+      wf[fn] = u32x4{w0[0], w0[1], w1[0], w1[1]};
+    }
+  };
+  auto mfmas = [&]() {
+    __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn) {
 #pragma unroll
       for (int fm = 0; fm < FM; ++fm) {
         if constexpr (kI8)
-          acc[fn][fm] = mfma_i8_k64(wf, xf[fm], acc[fn][fm]);
+          acc[fn][fm] = mfma_i8_k64(wf[fn], xf[fm], acc[fn][fm]);
         else
-          acc[fn][fm] = mfma_k32(DT, wf, xf[fm], acc[fn][fm]);
+          acc[fn][fm] = mfma_k32(DT, wf[fn], xf[fm], acc[fn][fm]);
       }
     }
+    __builtin_amdgcn_s_setprio(0);
+  };
+  auto next_slot = [](int s0) { return s0 + 1 == kRing ? 0 : s0 + 1; };
+  auto prev_slot = [](int s0) { return s0 == 0 ? kRing - 1 : s0 - 1; };
+  // Wait until this wave's loads of a stage are complete while `later` of
+  // its loads of later stages stay in flight, then barrier.
+  auto wait_stage = [&](int later) {
+    if (later >= 3)
+      vm_wait_barrier<3 * kDma>();
+    else if (later == 2)
+      vm_wait_barrier<2 * kDma>();
+    else if (later == 1)
+      vm_wait_barrier<kDma>();
+    else
+      vm_wait_barrier<0>();
+  };
+  auto later_after = [&](int t) {   // loads of stages after t+1 in flight at the end of A(t)
+    const int l = nk - 2 - t;
+    return l < kRing - 2 ? l : kRing - 2;
   };
 
-  // One K step from ring slot S (= t mod 4): wait until this wave's loads
-  // of the step are done (kWait later loads may stay in flight), barrier
-  // (every wave's part is visible, and every wave is done with the slot of
-  // step t-1), refill that slot with step t+3 if kRefill, compute.
-  auto step = [&](auto S, auto kWait, auto kRefill, int t) {
-    constexpr int s = decltype(S)::value;
-    ring_barrier<decltype(kWait)::value>();
-    if constexpr (decltype(kRefill)::value) issue((s + 3) & 3, t + 3);
-    compute(s);
-  };
-  using I0 = std::integral_constant<int, 0>;
-  using I1 = std::integral_constant<int, 1>;
-  using I2 = std::integral_constant<int, 2>;
-  using I3 = std::integral_constant<int, 3>;
-  using W2 = std::integral_constant<int, 2 * kLoadsPerStage>;
-  using W1 = std::integral_constant<int, kLoadsPerStage>;
-  using W0 = std::integral_constant<int, 0>;
-  using Yes = std::true_type;
-  using No = std::false_type;
-
-  // nk is a multiple of 4 here (N % 256 == 0).  Steady state: branch-free.
-  issue(0, 0);
-  issue(1, 1);
-  issue(2, 2);
-  int t = 0;
-  for (; t < nk - 4; t += 4) {
-    step(I0{}, W2{}, Yes{}, t);
-    step(I1{}, W2{}, Yes{}, t + 1);
-    step(I2{}, W2{}, Yes{}, t + 2);
-    step(I3{}, W2{}, Yes{}, t + 3);
+  for (int s0 = 0; s0 < kRing; ++s0)
+    if (s0 < nk) issue(s0, s0);
+  wait_stage(nk - 1 < kRing - 1 ? nk - 1 : kRing - 1);
+  int slot = 0;
+  if (grp == 0) {
+    read_frags(0);
+    for (int t = 0; t < nk; ++t) {
+      mfmas();                                            // A(t): compute stage t
+      wait_stage(later_after(t));
+      if (t + kRing < nk) issue(slot, t + kRing);         // B(t): refill, read t+1
+      if (t + 1 < nk) read_frags(next_slot(slot));
+      vm_wait_barrier<63>();
+      slot = next_slot(slot);
+    }
+  } else {
+    for (int t = 0; t < nk; ++t) {
+      if (t >= 1 && t - 1 + kRing < nk) issue(prev_slot(slot), t - 1 + kRing);
+      read_frags(slot);                                   // A(t): refill, read t
+      wait_stage(later_after(t));
+      mfmas();                                            // B(t): compute stage t
+      vm_wait_barrier<63>();
+      slot = next_slot(slot);
+    }
   }
-  // Last four steps: stage nk-1 is the final refill.
-  step(I0{}, W2{}, Yes{}, t);
-  step(I1{}, W2{}, No{}, t + 1);
-  step(I2{}, W1{}, No{}, t + 2);
-  step(I3{}, W0{}, No{}, t + 3);
 
   // Epilogue: lane holds C[row][col .. col+3] of every accumulator block.
 #pragma unroll
   for (int fn = 0; fn < FN; ++fn) {
 #pragma unroll
     for (int fm = 0; fm < FM; ++fm) {
-      const int row = m0 + wm * 128 + fm * 16 + r;
-      const int col = n0 + wn * 128 + fn * 16 + 4 * g;
+      const int row = m0 + grp * 128 + fm * 16 + r;
+      const int col = n0 + q * 64 + fn * 16 + 4 * g;
       if constexpr (DT == TCU_BF16_BF16) {
         const f32x4 v = acc[fn][fm];
         *(u32x2 *)(C + ((int64_t)row * N + col) * 2) =
@@ -453,7 +480,7 @@ hipError_t launch_cfg(const void *A, const void *B, void *C, int64_t N, hipStrea
   return hipGetLastError();
 }
 
-// Kernel selection: TCU_GEMM_KERNEL=fast forces the full-tile kernel
+// Kernel selection: TCU_GEMM_KERNEL=fast forces the full-tile (ping-pong) kernel
 // wherever N % 256 == 0, =general forces the general kernel; unset or
 // =auto picks by size.
 enum class GemmPath { kAuto, kFast, kGeneral };
@@ -474,7 +501,7 @@ hipError_t launch_dt(const void *A, const void *B, void *C, int64_t N, hipStream
   const bool fast_ok = (N % 256 == 0);
   if (fast_ok && (path == GemmPath::kFast || (path == GemmPath::kAuto && big_tiles >= num_cus))) {
     const int t = (int)(N / 256);
-    hipLaunchKernelGGL((gemm_fast_kernel<DT>), dim3(t * t), dim3(256), 0, stream,
+    hipLaunchKernelGGL((gemm_pp_kernel<DT, TCU_RING>), dim3(t * t), dim3(512), 0, stream,
                        (const unsigned char *)A, (const unsigned char *)B, (unsigned char *)C,
                        (int)N, t, t);
     return hipGetLastError();
