@@ -290,10 +290,15 @@ __device__ __forceinline__ int fb8_swz(int k) { return (k & 7) | (((k >> 4) & 1)
 // Stage t+1 must be complete when A(t) ends, so every wave waits there for
 // its own loads of stage t+1 before the barrier.
 // ---------------------------------------------------------------------------
+// Wait until at most n of this wave's DMA loads are in flight and all its
+// LDS reads have returned, then a workgroup barrier.  The barrier is an
+// instruction with a memory clobber: the compiler may not move LDS accesses
+// across it (the barrier intrinsic alone does not order memory), while no
+// memory fence -- which would drain every in-flight DMA -- is emitted.
 template <int n>
 __device__ __forceinline__ void vm_wait_barrier() {
   __builtin_amdgcn_s_waitcnt((n & 15) | (7 << 4) | (0 << 8) | (((n >> 4) & 3) << 14));
-  __builtin_amdgcn_s_barrier();
+  asm volatile("s_barrier" ::: "memory");
 }
 
 template <int DT, int kRing>
