@@ -26,9 +26,7 @@
 // 16x16x64 (int8) matrix-core instructions.  The product is formed as
 // C^T = B^T A^T so each lane holds 4 consecutive columns of one row of C,
 // stored as one 16-byte write.
-// Workgroup order is XCD-aware: consecutive workgroup ids land on different
-// XCDs, so ids are remapped to give each XCD a contiguous, grouped range of
-// tiles that share A row-panels and B column-panels in its private L2.
+// Workgroup order is XCD-aware (see map_tile).
 #include <cstdlib>
 #include <cstring>
 
@@ -39,10 +37,10 @@ namespace tcu {
 namespace {
 
 #ifndef TCU_GROUP_M
-#define TCU_GROUP_M 8
+#define TCU_GROUP_M 2
 #endif
 #ifndef TCU_XCD_REMAP
-#define TCU_XCD_REMAP 1
+#define TCU_XCD_REMAP 0
 #endif
 #ifndef TCU_RING
 #define TCU_RING 5
@@ -52,7 +50,13 @@ constexpr int kBKB = 128;  // bytes of the contracted index per K-step and LDS r
 
 __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row ^ (row >> 3)) & 7); }
 
-// Map a workgroup id to an output tile (tm, tn).
+// Map a workgroup id to an output tile (tm, tn): groups of TCU_GROUP_M tile
+// rows are walked column by column.  Consecutive workgroup ids are dispatched
+// round-robin over the 8 XCDs, so with groups of 2 rows each XCD's concurrent
+// workgroups cover a compact block of tiles (shared A row-panels and B
+// column-panels in its L2) while all XCDs together sweep a band of full rows
+// (B panels shared through the memory-side cache).  Measured best for N=8192
+// against larger groups and an explicit per-XCD remap (TCU_XCD_REMAP=1).
 __device__ __forceinline__ void map_tile(int pid, int tiles_m, int tiles_n, int &tm, int &tn) {
   const int total = tiles_m * tiles_n;
   constexpr int kXcds = 8;
