@@ -504,7 +504,7 @@ GemmPath gemm_path() {
 template <int DT>
 hipError_t launch_dt(const void *A, const void *B, void *C, int64_t N, hipStream_t stream,
                      int num_cus) {
-  // Big tiles when they fill the chip; otherwise smaller tiles for more workgroups.
+  // The largest tiles that still give every CU a workgroup.
   const int64_t big_tiles = ((N + 255) / 256) * ((N + 255) / 256);
   const GemmPath path = gemm_path();
   const bool fast_ok = (N % 256 == 0);
@@ -516,7 +516,9 @@ hipError_t launch_dt(const void *A, const void *B, void *C, int64_t N, hipStream
     return hipGetLastError();
   }
   if (big_tiles >= num_cus) return launch_cfg<DT, 256, 256, 2, 2>(A, B, C, N, stream);
-  return launch_cfg<DT, 128, 128, 2, 2>(A, B, C, N, stream);
+  const int64_t mid_tiles = ((N + 127) / 128) * ((N + 127) / 128);
+  if (mid_tiles >= num_cus) return launch_cfg<DT, 128, 128, 2, 2>(A, B, C, N, stream);
+  return launch_cfg<DT, 64, 64, 2, 2>(A, B, C, N, stream);
 }
 
 }  // namespace

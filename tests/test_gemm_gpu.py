@@ -24,7 +24,7 @@ def test_workload_f16_N1024_s16():
 
 # sizes spanning 1, several and ragged tiles (N is always a multiple of s)
 SIZES = [(16, 16), (32, 16), (48, 16), (32, 32), (64, 32), (96, 32), (272, 16),
-         (400, 16), (544, 32), (1056, 32)]
+         (400, 16), (544, 32), (1056, 32), (2080, 32)]
 
 
 @pytest.mark.parametrize("din,dout", DTYPES)
