@@ -13,6 +13,11 @@ numpy in/out:
   A so that large cases can be checked on sampled rows.
 * ``f16_to_f64``, ``bf16_to_f64`` -- format decoders.
 * ``f64_to_bf16`` -- one-step round-to-nearest-even to bfloat16 bit patterns.
+* ``mm_acc(A, B, C0, dtype, out)`` -- the accumulating form ``C0 + A*B``
+  that the D functions of Sections 4.2 and 4.3 ask of the unit
+  (X <- X + Y*Z); C0 holds stored output values ('f32', 'bf16' bits or
+  'i32').  Rectangular shapes (Corollary 1) need nothing new: ``mm`` takes
+  any (R x K) times (K x J).
 
 Every function here is pinned by tests/test_oracle_pins.py against values the
 mathematics fixes (exact rational brute force, closed forms, library
@@ -123,3 +128,23 @@ def mm(A: np.ndarray, B: np.ndarray, dtype: str, rows=None) -> np.ndarray:
     if rc != 0:
         raise ValueError("oracle rejected its arguments")
     return out
+
+
+def decode_out(C0: np.ndarray, out: str) -> np.ndarray:
+    """Stored output values as float64 (or int64 for 'i32')."""
+    if out == "i32":
+        return np.asarray(C0, dtype=np.int32).astype(np.int64)
+    if out == "bf16":
+        return bf16_to_f64(np.ascontiguousarray(C0).view(np.uint16))
+    return np.asarray(C0, dtype=np.float32).astype(np.float64)
+
+
+def mm_acc(A: np.ndarray, B: np.ndarray, C0: np.ndarray, dtype: str, out: str,
+           rows=None) -> np.ndarray:
+    """C0 + A*B for the selected rows, summed exactly in binary64 (or int64);
+    the caller rounds once to the output format."""
+    prod = mm(A, B, dtype, rows=rows)
+    c0 = decode_out(C0, out)
+    if rows is not None:
+        c0 = c0[np.asarray(rows, dtype=np.int64)]
+    return c0 + prod

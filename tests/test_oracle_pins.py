@@ -379,3 +379,62 @@ def test_pins_catch_planted_mistakes(oracle_mod):
             out = mut(A, B, dt)
             return np.full((A.shape[0], B.shape[1]), np.nan) if out is None else out
         assert not check_closed_form(fn, "i8"), mut.__name__
+
+
+# ---------------------------------------- accumulate and rectangular forms
+def test_mm_rectangular_vs_exact(oracle_mod):
+    """Corollary 1's rectangular product is the same definition."""
+    for (R, K, J, dt) in [(5, 48, 16, "bf16"), (33, 16, 64, "f16"), (17, 96, 32, "i8")]:
+        A = gen_bits((R, K), dt, "int8" if dt == "i8" else "normal", R + K)
+        B = gen_bits((K, J), dt, "int8" if dt == "i8" else "normal", J + K)
+        got = oracle_mod.mm(A, B, dt)
+        ex = exact_mm(A, B, dt)
+        if dt == "i8":
+            assert got.tolist() == ex
+        else:
+            absab = abs_mm(A, B, dt)
+            for r in range(R):
+                for j in range(J):
+                    err = abs(Fraction(float(got[r, j])) - ex[r][j])
+                    assert err <= Fraction(K * 2.0 ** -52) * Fraction(float(absab[r, j]))
+
+
+def test_mm_acc_zero_start_equals_product(oracle_mod):
+    A = gen_bits((40, 32), "bf16", "normal", 61)
+    B = gen_bits((32, 48), "bf16", "normal", 62)
+    z32 = np.zeros((40, 48), dtype=np.float32)
+    assert np.array_equal(oracle_mod.mm_acc(A, B, z32, "bf16", "f32"), oracle_mod.mm(A, B, "bf16"))
+    zbf = np.zeros((40, 48), dtype=np.uint16)
+    assert np.array_equal(oracle_mod.mm_acc(A, B, zbf, "bf16", "bf16"), oracle_mod.mm(A, B, "bf16"))
+
+
+def test_mm_acc_linearity_small_ints(oracle_mod):
+    """(A B1) accumulated onto by A B2 equals A (B1 + B2): exact for small ints."""
+    for dt, out in (("i8", "i32"), ("f16", "f32"), ("bf16", "bf16")):
+        A = inputs.bits(inputs.small_ints((24, 32), dt, 71))
+        B1t = inputs.small_ints((32, 16), dt, 72)
+        B2t = inputs.small_ints((32, 16), dt, 73)
+        B1, B2 = inputs.bits(B1t), inputs.bits(B2t)
+        Bsum = inputs.bits((B1t.to(torch.float32) + B2t.to(torch.float32)).to(inputs.TORCH_DTYPE[dt]))
+        first = oracle_mod.mm(A, B1, dt)
+        if out == "i32":
+            c0 = first.astype(np.int32)
+        elif out == "bf16":
+            c0 = oracle_mod.f64_to_bf16(first)
+        else:
+            c0 = first.astype(np.float32)
+        got = oracle_mod.mm_acc(A, B2, c0, dt, out)
+        assert np.array_equal(np.asarray(got, dtype=np.float64),
+                              np.asarray(oracle_mod.mm(A, Bsum, dt), dtype=np.float64))
+
+
+def test_mm_acc_cancellation_and_rows(oracle_mod):
+    """C0 = -A B accumulates to exactly zero; row selection is consistent."""
+    A = gen_bits((30, 16), "i8", "int8", 81)
+    B = gen_bits((16, 32), "i8", "int8", 82)
+    neg = (-oracle_mod.mm(A, B, "i8")).astype(np.int32)
+    assert not np.any(oracle_mod.mm_acc(A, B, neg, "i8", "i32"))
+    rows = np.array([3, 0, 29])
+    c0 = np.arange(30 * 32, dtype=np.int32).reshape(30, 32)
+    full = oracle_mod.mm_acc(A, B, c0, "i8", "i32")
+    assert np.array_equal(oracle_mod.mm_acc(A, B, c0, "i8", "i32", rows=rows), full[rows])
