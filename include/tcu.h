@@ -20,12 +20,13 @@
  *
  * Conventions shared by every entry point:
  *   - All matrix pointers are DEVICE pointers (memory of the current HIP
- *     device).  Matrices are row-major and contiguous: element (r, c) of an
- *     R x C matrix is at index r*C + c.
+ *     device).  Matrices are row-major; element (r, c) of an R x C matrix
+ *     is at index r*ld + c, with ld = C (contiguous) except where an entry
+ *     point takes an explicit row pitch ld (tcu_gemm_rect).
  *   - The caller allocates and frees A, B and C.  The library never
  *     allocates, frees or retains them, and keeps no pointer across calls.
- *   - C is overwritten with the product (the unit stores its result; it does
- *     not accumulate into C).
+ *   - C is overwritten with the product (the unit stores its result), except
+ *     in the accumulating form of tcu_gemm_rect.
  *   - Calls are asynchronous on the stream in effect; the caller synchronises.
  *   - Every call returns a tcu_status: 0 on success, a negative code on
  *     failure.  Argument checks (null, shape, unit size, dtype, alignment,
@@ -129,6 +130,62 @@ int tcu_mm_tall_ex(const void *A, int64_t n, int s, const void *B, void *C,
                    int dtype, void *hip_stream);
 int tcu_gemm_ex(const void *A, const void *B, void *C, int64_t N, int s,
                 int dtype, void *hip_stream);
+
+/* ---- rectangular, strided and accumulating product ----
+ *
+ * C (M x N) = A (M x K) * B (K x N)                      (flags = 0)
+ * C (M x N) = C + A (M x K) * B (K x N)                  (flags = TCU_ACCUMULATE)
+ *
+ * Corollary 1 (Section 4.1) multiplies a sqrt(n) x r matrix by an
+ * r x sqrt(n) one by cutting it into unit-sized pieces and applying
+ * Theorem 2.  This entry point does exactly that for any M, K, N: A is cut
+ * into M x s vertical strips A_i (i < ceil(K/s)), B into s x s blocks
+ * B_{i,j} (j < ceil(N/s)), and output strip j is sum_i A_i * B_{i,j}, so
+ * it issues ceil(K/s) * ceil(N/s) tall calls with n = M rows (the bound
+ * r*sqrt(n)/m of Corollary 1 when M = N = sqrt(n), K = r).  Dimensions
+ * that are not multiples of s are zero-padded: the missing rows and columns
+ * of the last strip and blocks are taken as zeros, which leaves the
+ * product unchanged; nothing outside the M x N output is written.
+ * The accumulating form is the update X <- X + Y * Z that the D functions
+ * of the Gaussian-elimination and transitive-closure algorithms
+ * (Sections 4.2 and 4.3) ask of the unit.
+ *
+ *   A: M x K input elements, row r at A + r*lda elements (lda >= K).
+ *   B: K x N input elements, row k at B + k*ldb elements (ldb >= N).
+ *   C: M x N output elements, row r at C + r*ldc elements (ldc >= N); read
+ *      too when accumulating.  The three matrices may be views into larger
+ *      row-major arrays.
+ *   M, K, N: 0 <= M, K, N <= TCU_MAX_RECT_DIM.  M = 0 or N = 0 is a no-op;
+ *      K = 0 writes zeros (flags = 0) or leaves C unchanged (accumulate).
+ *   flags: 0 or TCU_ACCUMULATE.
+ * A, B or C may be NULL when that matrix has no elements (M*K, K*N or M*N
+ * is 0); otherwise NULL is TCU_ERR_NULL.
+ * Arithmetic: the sum over K is formed in binary32 (int32 for int8
+ * inputs); when accumulating, the stored C value is added to it in the
+ * same type and the result is stored once (rounded to nearest even for a
+ * bfloat16 output).  For int8 inputs K < 2^17 is required, so A*B is exact
+ * in int32; the accumulated C + A*B wraps modulo 2^32 if it leaves the
+ * int32 range.
+ * Layout rules: base pointers 16-byte aligned; every element each operand
+ * addresses must lie below 2^40 bytes from its base.  Row pitches need no
+ * alignment, but pitches whose byte size is a multiple of 16 (lda, ldb, ldc
+ * multiples of 8 for 16-bit, of 16 for int8, of 4 for 32-bit elements) take
+ * the vector-load kernels; others use element-wise loads.  C must not share
+ * an element with A or B: views of one array with the same byte pitch are
+ * checked element-exactly, other cases by address range.
+ * Errors: TCU_ERR_NULL, TCU_ERR_SHAPE (a dimension out of range, int8 with
+ * K >= 2^17, a pitch below its row length, an extent of 2^40 bytes or more),
+ * TCU_ERR_UNSUPPORTED (unit size, dtype or flags), TCU_ERR_ALIGN,
+ * TCU_ERR_OVERLAP, TCU_ERR_NO_DEVICE, TCU_ERR_HIP.
+ * Cost accounting: ceil(K/s)*ceil(N/s) calls, each of ceil(M/s) square
+ * calls and ceil(M/s)*s*s work (0 of each if M, K or N is 0). */
+#define TCU_ACCUMULATE 1
+#define TCU_MAX_RECT_DIM ((int64_t)1 << 30)
+int tcu_gemm_rect(const void *A, int64_t lda, const void *B, int64_t ldb, void *C, int64_t ldc,
+                  int64_t M, int64_t K, int64_t N, int flags);
+int tcu_gemm_rect_ex(const void *A, int64_t lda, const void *B, int64_t ldb, void *C,
+                     int64_t ldc, int64_t M, int64_t K, int64_t N, int flags, int s, int dtype,
+                     void *hip_stream);
 
 /* ---- cost accounting (Theorem 2 proof; Section 5 weak model) ----
  * tcu_calls:        logical tensor-unit calls issued (1 per tall call,

@@ -21,7 +21,7 @@ from __future__ import annotations
 
 import numpy as np
 
-from . import f64_to_bf16, bf16_to_f64, mm
+from . import decode_out, f64_to_bf16, bf16_to_f64, mm, mm_acc
 
 REL_FROB = 1e-3
 ELEM = 1e-2
@@ -96,13 +96,34 @@ def check_exact(got, ref) -> dict:
     return {"mismatches": 0}
 
 
-def check(dtype_in: str, dtype_out: str, A_bits, B_bits, got, rows=None) -> dict:
+def wrap_i32(x: np.ndarray) -> np.ndarray:
+    """Exact integers reduced to int32 two's complement (wrap-around)."""
+    x = np.asarray(x, dtype=np.int64)
+    return ((x + 2 ** 31) % 2 ** 32) - 2 ** 31
+
+
+def check(dtype_in: str, dtype_out: str, A_bits, B_bits, got, rows=None, C0=None) -> dict:
     """Compare a GPU result (numpy; bf16 output as uint16 bits) with the oracle
-    on the given rows of A (all rows when None)."""
-    ref = mm(A_bits, B_bits, dtype_in, rows=rows)
+    on the given rows of A (all rows when None).
+
+    C0: the stored output before an accumulating call (full matrix, stored
+    values: float32, bf16 bits or int32); the reference is then C0 + A*B,
+    the binary32 (or int32) addition of C0 counting as one more term of
+    the sum in the error bounds, whose magnitude term becomes
+    |A| |B| + |C0|.  int32 results are compared modulo 2^32, the documented
+    wrap-around of the accumulating form."""
+    if C0 is None:
+        ref = mm(A_bits, B_bits, dtype_in, rows=rows)
+    else:
+        ref = mm_acc(A_bits, B_bits, C0, dtype_in, dtype_out, rows=rows)
     if dtype_in == "i8":
-        return check_exact(got, ref)
+        return check_exact(got, wrap_i32(ref) if C0 is not None else ref)
     absab = mm(abs_bits(A_bits), abs_bits(B_bits), dtype_in, rows=rows)
+    K = np.asarray(A_bits).shape[1]
+    if C0 is not None:
+        c0 = np.abs(decode_out(C0, dtype_out))
+        absab = absab + (c0 if rows is None else c0[np.asarray(rows, dtype=np.int64)])
+        K += 1
     if dtype_out == "bf16":
-        return check_bf16(got, ref, absab, K=np.asarray(A_bits).shape[1])
+        return check_bf16(got, ref, absab, K=K)
     return check_float(got, ref, absab)

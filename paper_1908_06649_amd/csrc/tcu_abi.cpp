@@ -103,6 +103,70 @@ int validate_gemm(const void *A, const void *B, const void *C, int64_t N, int s,
   return TCU_OK;
 }
 
+// Bytes from the base of an R x C view with row pitch ld (elements of es
+// bytes) to one past its last element; 0 for an empty view.  Inputs are
+// bounded (R, C <= 2^30, ld < 2^40) so the product cannot overflow.
+int64_t view_extent(int64_t rows, int64_t cols, int64_t ld, int64_t es) {
+  if (rows == 0 || cols == 0) return 0;
+  return ((rows - 1) * ld + cols) * es;
+}
+
+// Whether two row-major views (base, rows, bytes per row, byte pitch) share
+// a byte.  Disjoint address ranges never do.  Views with one byte pitch P
+// (a single-row view takes the other's pitch) are laid on one grid of
+// P-byte rows and tested as rectangles, so disjoint blocks of one array
+// (the D functions of Sections 4.2 and 4.3 work on such blocks) pass.
+// Other overlapping ranges are reported as overlapping.
+bool views_overlap(const void *a, int64_t ar, int64_t aw, int64_t ap, const void *b, int64_t br,
+                   int64_t bw, int64_t bp) {
+  if (ar == 0 || aw == 0 || br == 0 || bw == 0) return false;
+  if (!overlap(a, (ar - 1) * ap + aw, b, (br - 1) * bp + bw)) return false;
+  if (ar == 1 && br == 1) return true;
+  if (ar == 1 && aw <= bp) ap = bp;
+  if (br == 1 && bw <= ap) bp = ap;
+  if (ap != bp) return true;
+  const int64_t P = ap;
+  const int64_t d = (int64_t)(reinterpret_cast<uintptr_t>(b) - reinterpret_cast<uintptr_t>(a));
+  int64_t q = d / P, c = d % P;
+  if (c < 0) {
+    c += P;
+    q -= 1;
+  }
+  // In a's grid, row i of b covers bytes [c, c + bw) of grid row q + i,
+  // continuing into grid row q + i + 1 when c + bw > P.
+  auto hits = [&](int64_t r0, int64_t c0, int64_t c1) {
+    return r0 < ar && r0 + br > 0 && c0 < aw && c1 > 0;
+  };
+  if (hits(q, c, c + bw < P ? c + bw : P)) return true;
+  return c + bw > P && hits(q + 1, 0, c + bw - P);
+}
+
+int validate_rect(const void *A, int64_t lda, const void *B, int64_t ldb, const void *C,
+                  int64_t ldc, int64_t M, int64_t K, int64_t N, int flags, int s, int dt) {
+  if (!unit_ok(s) || !dtype_ok(dt) || (flags & ~TCU_ACCUMULATE) != 0) return TCU_ERR_UNSUPPORTED;
+  if (M < 0 || K < 0 || N < 0 || M > TCU_MAX_RECT_DIM || K > TCU_MAX_RECT_DIM ||
+      N > TCU_MAX_RECT_DIM)
+    return TCU_ERR_SHAPE;
+  // A pointer may be NULL only if its matrix has no elements.
+  if ((!A && M * K > 0) || (!B && K * N > 0) || (!C && M * N > 0)) return TCU_ERR_NULL;
+  // int32 sums of K products of magnitude <= 2^14 stay exact while K < 2^17.
+  if (dt == TCU_I8_I32 && K >= ((int64_t)1 << 17)) return TCU_ERR_SHAPE;
+  constexpr int64_t kMaxExtent = (int64_t)1 << 40;
+  if (lda < K || ldb < N || ldc < N || lda >= kMaxExtent || ldb >= kMaxExtent ||
+      ldc >= kMaxExtent)
+    return TCU_ERR_SHAPE;
+  const int64_t ea = view_extent(M, K, lda, in_size(dt));
+  const int64_t eb = view_extent(K, N, ldb, in_size(dt));
+  const int64_t ec = view_extent(M, N, ldc, out_size(dt));
+  if (ea >= kMaxExtent || eb >= kMaxExtent || ec >= kMaxExtent) return TCU_ERR_SHAPE;
+  if (misaligned(A) || misaligned(B) || misaligned(C)) return TCU_ERR_ALIGN;
+  const int64_t ci = in_size(dt), co = out_size(dt);
+  if (views_overlap(C, M, N * co, ldc * co, A, M, K * ci, lda * ci) ||
+      views_overlap(C, M, N * co, ldc * co, B, K, N * ci, ldb * ci))
+    return TCU_ERR_OVERLAP;
+  return TCU_OK;
+}
+
 }  // namespace
 
 TCU_EXPORT int tcu_set_unit(int s) {
@@ -132,7 +196,8 @@ TCU_EXPORT int tcu_mm_tall_ex(const void *A, int64_t n, int s, const void *B, vo
   int num_cus = 0;
   rc = device_ready(&num_cus);
   if (rc != TCU_OK) return rc;
-  if (tcu::launch_tall(dtype, s, A, n, B, C, (hipStream_t)hip_stream, num_cus) != hipSuccess)
+  if (tcu::launch_tall(dtype, s, A, n, B, C, false, (hipStream_t)hip_stream, num_cus) !=
+      hipSuccess)
     return TCU_ERR_HIP;
   g_calls.fetch_add(1, std::memory_order_relaxed);
   g_square_calls.fetch_add((n + s - 1) / s, std::memory_order_relaxed);
@@ -153,7 +218,8 @@ TCU_EXPORT int tcu_gemm_ex(const void *A, const void *B, void *C, int64_t N, int
   int num_cus = 0;
   rc = device_ready(&num_cus);
   if (rc != TCU_OK) return rc;
-  if (tcu::launch_gemm(dtype, A, B, C, N, (hipStream_t)hip_stream, num_cus) != hipSuccess)
+  const tcu::RectArgs args{A, N, B, N, C, N, N, N, N, false};
+  if (tcu::launch_rect(dtype, s, args, (hipStream_t)hip_stream, num_cus) != hipSuccess)
     return TCU_ERR_HIP;
   // Theorem 2: (N/s)^2 calls, each on an N x s strip (N/s weak-model square
   // calls and N*s model work apiece).
@@ -166,6 +232,37 @@ TCU_EXPORT int tcu_gemm_ex(const void *A, const void *B, void *C, int64_t N, int
 
 TCU_EXPORT int tcu_gemm(const void *A, const void *B, void *C, int64_t N) {
   return tcu_gemm_ex(A, B, C, N, g_cfg.s, g_cfg.dtype, g_cfg.stream);
+}
+
+TCU_EXPORT int tcu_gemm_rect_ex(const void *A, int64_t lda, const void *B, int64_t ldb, void *C,
+                                int64_t ldc, int64_t M, int64_t K, int64_t N, int flags, int s,
+                                int dtype, void *hip_stream) {
+  int rc = validate_rect(A, lda, B, ldb, C, ldc, M, K, N, flags, s, dtype);
+  if (rc != TCU_OK) return rc;
+  const bool accum = (flags & TCU_ACCUMULATE) != 0;
+  // Nothing to store, or C + (empty sum) = C.
+  if (M == 0 || N == 0 || (K == 0 && accum)) return TCU_OK;
+  int num_cus = 0;
+  rc = device_ready(&num_cus);
+  if (rc != TCU_OK) return rc;
+  const tcu::RectArgs args{A, lda, B, ldb, C, ldc, M, K, N, accum};
+  if (tcu::launch_rect(dtype, s, args, (hipStream_t)hip_stream, num_cus) != hipSuccess)
+    return TCU_ERR_HIP;
+  // Corollary 1 via Theorem 2 on the zero-padded operands: ceil(K/s) strips
+  // times ceil(N/s) blocks per strip, one call each, every call on all
+  // ceil(M/s)*s padded rows.
+  const int64_t calls = ((K + s - 1) / s) * ((N + s - 1) / s);
+  const int64_t row_blocks = (M + s - 1) / s;
+  g_calls.fetch_add(calls, std::memory_order_relaxed);
+  g_square_calls.fetch_add(calls * row_blocks, std::memory_order_relaxed);
+  g_work.fetch_add(calls * row_blocks * s * s, std::memory_order_relaxed);
+  return TCU_OK;
+}
+
+TCU_EXPORT int tcu_gemm_rect(const void *A, int64_t lda, const void *B, int64_t ldb, void *C,
+                             int64_t ldc, int64_t M, int64_t K, int64_t N, int flags) {
+  return tcu_gemm_rect_ex(A, lda, B, ldb, C, ldc, M, K, N, flags, g_cfg.s, g_cfg.dtype,
+                          g_cfg.stream);
 }
 
 TCU_EXPORT int64_t tcu_calls(void) { return g_calls.load(std::memory_order_relaxed); }

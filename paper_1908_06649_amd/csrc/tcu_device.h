@@ -130,4 +130,88 @@ __device__ __forceinline__ unsigned pack_bf16x2(float lo, float hi) {
   return (unsigned)bitcast<unsigned short>(a) | ((unsigned)bitcast<unsigned short>(b) << 16);
 }
 
+// bfloat16 bit pattern -> binary32 (exact).
+__device__ __forceinline__ float bf16_to_f32(unsigned bits16) {
+  return __builtin_bit_cast(float, bits16 << 16);
+}
+
+// One 16-byte chunk of EPC elements of ES bytes at p, of which the first
+// `valid` (0..EPC) lie inside the matrix; the others are returned as zero
+// (the zero padding of a partial strip or block) and are not read.  kVec:
+// p is 16-byte aligned, so a full chunk is one vector load.
+template <int ES, bool kVec>
+__device__ __forceinline__ u32x4 load_chunk(const unsigned char *p, int valid) {
+  constexpr int EPC = 16 / ES;
+  if (kVec && valid >= EPC) return *(const u32x4 *)p;
+  u32x4 v = {0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int e = 0; e < EPC; ++e) {
+    if (e < valid) {
+      const unsigned x = ES == 2 ? (unsigned)((const unsigned short *)p)[e] : (unsigned)p[e];
+      v[(e * ES) >> 2] |= x << (8 * ((e * ES) & 3));
+    }
+  }
+  return v;
+}
+
+// Store 4 consecutive output values of one row of C at p (element col of
+// the row), of which the first `valid` (0..4) lie inside the matrix.  With
+// acc the stored values are read and added first (binary32 or int32 sum,
+// one rounding to the output type).  kVec: p is aligned for one vector
+// access of the 4 values.
+template <int DT, bool kVec, typename Acc>
+__device__ __forceinline__ void store_out4(unsigned char *p, Acc v, int valid, bool acc) {
+  if constexpr (DT == TCU_BF16_BF16) {
+    unsigned short *q = (unsigned short *)p;
+    if (kVec && valid >= 4) {
+      if (acc) {
+        const u32x2 o = *(const u32x2 *)p;
+        v[0] += bf16_to_f32(o[0] & 0xffffu);
+        v[1] += bf16_to_f32(o[0] >> 16);
+        v[2] += bf16_to_f32(o[1] & 0xffffu);
+        v[3] += bf16_to_f32(o[1] >> 16);
+      }
+      *(u32x2 *)p = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        if (e < valid) {
+          float x = v[e];
+          if (acc) x += bf16_to_f32(q[e]);
+          q[e] = (unsigned short)(pack_bf16x2(x, 0.f) & 0xffffu);
+        }
+      }
+    }
+  } else {
+    // int32 sums are formed as unsigned words: two's-complement wrap-around.
+    constexpr bool kInt = (DT == TCU_I8_I32);
+    if (kVec && valid >= 4) {
+      u32x4 w = bitcast<u32x4>(v);
+      if (acc) {
+        const u32x4 o = *(const u32x4 *)p;
+        if constexpr (kInt)
+          w += o;
+        else
+          w = bitcast<u32x4>(bitcast<f32x4>(w) + bitcast<f32x4>(o));
+      }
+      *(u32x4 *)p = w;
+    } else {
+      unsigned *q = (unsigned *)p;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        if (e < valid) {
+          unsigned w = bitcast<unsigned>(v[e]);
+          if (acc) {
+            if constexpr (kInt)
+              w += q[e];
+            else
+              w = bitcast<unsigned>(bitcast<float>(w) + bitcast<float>(q[e]));
+          }
+          q[e] = w;
+        }
+      }
+    }
+  }
+}
+
 }  // namespace tcu

@@ -71,14 +71,22 @@ __device__ __forceinline__ void map_tile(int pid, int tiles_m, int tiles_n, int 
   tn = in_group / gsz;
 }
 
-template <int DT, int BM, int BN, int WM, int WN>
+// C (M x N) = A (M x K) * B (K x N) [+ C when accum], operands with row
+// pitches lda, ldb, ldc (elements).  Rows, columns and contracted indices
+// beyond M, N, K are zero padding: chunks reaching past an edge are loaded
+// element by element with zeros in place of the missing elements, and only
+// in-range outputs are stored.  kVec: every pitch is a multiple of 16 bytes
+// (full chunks are vector loads, 4-value groups of C vector accesses).
+template <int DT, int BM, int BN, int WM, int WN, bool kVec>
 __global__ __attribute__((amdgpu_flat_work_group_size(64 * WM * WN, 64 * WM * WN),
                           amdgpu_waves_per_eu(1, 1))) void
 gemm_kernel(const unsigned char *__restrict__ A, const unsigned char *__restrict__ B,
-            unsigned char *__restrict__ C, int N, int tiles_m, int tiles_n) {
+            unsigned char *__restrict__ C, int M, int N, int K, int64_t lda, int64_t ldb,
+            int64_t ldc, int accum, int tiles_m, int tiles_n) {
   constexpr bool kI8 = (DT == TCU_I8_I32);
   constexpr int NT = 64 * WM * WN;
   constexpr int ES = in_bytes(DT);
+  constexpr int OB = out_bytes(DT);
   constexpr int BK = kBKB / ES;                // contracted elements per K-step
   constexpr int EPC = 16 / ES;                 // elements per 16-byte chunk
   constexpr int CA = BM * 8 / NT;              // A chunks per thread
@@ -97,7 +105,7 @@ gemm_kernel(const unsigned char *__restrict__ A, const unsigned char *__restrict
   int tm, tn;
   map_tile(blockIdx.x, tiles_m, tiles_n, tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
-  const int64_t ld = (int64_t)N * ES;  // bytes per row of A and B
+  const int64_t lda_b = lda * ES, ldb_b = ldb * ES, ldc_b = ldc * OB;  // row pitches in bytes
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wid = tid >> 6;
@@ -112,28 +120,27 @@ gemm_kernel(const unsigned char *__restrict__ A, const unsigned char *__restrict
 
   u32x4 ra[CA];
   u32x4 rb[CB][8];
-  const u32x4 zero = {0u, 0u, 0u, 0u};
 
   // ---- global -> registers for the K-step starting at element k0 ----
   auto gload = [&](int k0) {
 #pragma unroll
     for (int i = 0; i < CA; ++i) {
       const int q = tid + NT * i;
-      const int row = q >> 3, c = q & 7;
-      const bool ok = (m0 + row < N) && (k0 + c * EPC < N);
-      ra[i] = ok ? *(const u32x4 *)(A + (int64_t)(m0 + row) * ld + (int64_t)k0 * ES + c * 16) : zero;
+      const int row = m0 + (q >> 3), kc = k0 + (q & 7) * EPC;
+      const int valid = row < M ? min(max(K - kc, 0), EPC) : 0;
+      ra[i] = load_chunk<ES, kVec>(A + (int64_t)row * lda_b + (int64_t)kc * ES, valid);
     }
 #pragma unroll
     for (int i = 0; i < CB; ++i) {
       const int q = tid + NT * i;
       const int nb = q % NBW, kb = q / NBW;
-      const bool okn = (q < NBLK) && (n0 + nb * EPC < N);
+      const int nc = n0 + nb * EPC;
+      const int nvalid = q < NBLK ? min(max(N - nc, 0), EPC) : 0;
 #pragma unroll
       for (int rr = 0; rr < 8; ++rr) {
         const int k = k0 + 8 * kb + rr;
-        rb[i][rr] = (okn && k < N)
-                        ? *(const u32x4 *)(B + (int64_t)k * ld + (int64_t)n0 * ES + nb * 16)
-                        : zero;
+        rb[i][rr] = load_chunk<ES, kVec>(B + (int64_t)k * ldb_b + (int64_t)nc * ES,
+                                         k < K ? nvalid : 0);
       }
     }
   };
@@ -217,7 +224,7 @@ gemm_kernel(const unsigned char *__restrict__ A, const unsigned char *__restrict
     }
   };
 
-  const int nk = (N + BK - 1) / BK;
+  const int nk = (K + BK - 1) / BK;
   gload(0);
   sstore(0);
   __syncthreads();
@@ -236,15 +243,10 @@ gemm_kernel(const unsigned char *__restrict__ A, const unsigned char *__restrict
     for (int fm = 0; fm < FM; ++fm) {
       const int row = m0 + wm * WTM + 16 * fm + r;
       const int col = n0 + wn * WTN + 16 * fn + 4 * g;
-      if (row < N && col < N) {
-        if constexpr (DT == TCU_BF16_BF16) {
-          const f32x4 v = acc[fn][fm];
-          *(u32x2 *)(C + ((int64_t)row * N + col) * 2) =
-              u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
-        } else {
-          *(u32x4 *)(C + ((int64_t)row * N + col) * 4) = bitcast<u32x4>(acc[fn][fm]);
-        }
-      }
+      const int valid = row < M ? min(max(N - col, 0), 4) : 0;
+      if (valid > 0)
+        store_out4<DT, kVec>(C + (int64_t)row * ldc_b + (int64_t)col * OB, acc[fn][fm], valid,
+                             accum != 0);
     }
   }
 }
@@ -308,9 +310,11 @@ __device__ __forceinline__ void vm_wait_barrier() {
 template <int DT, int kRing>
 __global__ __attribute__((amdgpu_flat_work_group_size(512, 512), amdgpu_waves_per_eu(2, 2))) void
 gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restrict__ B,
-               unsigned char *__restrict__ C, int N, int tiles_m, int tiles_n) {
+               unsigned char *__restrict__ C, int K, int64_t lda, int64_t ldb, int64_t ldc,
+               int accum, int tiles_m, int tiles_n) {
   constexpr bool kI8 = (DT == TCU_I8_I32);
   constexpr int ES = in_bytes(DT);
+  constexpr int OB = out_bytes(DT);
   constexpr int KE = kFastKB / ES;     // contracted elements per stage
   constexpr int BROW = 256 * ES;       // bytes per B row in a stage
   constexpr int FM = 8, FN = 4;        // 16 x 16 blocks per wave (128 x 64)
@@ -324,24 +328,24 @@ gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restr
   int tm, tn;
   map_tile(blockIdx.x, tiles_m, tiles_n, tm, tn);
   const int m0 = tm * 256, n0 = tn * 256;
-  const int64_t ld = (int64_t)N * ES;
+  const int64_t lda_b = lda * ES, ldb_b = ldb * ES, ldc_b = ldc * OB;
   const int lane = threadIdx.x & 63;
   const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int grp = wid >> 2, q = wid & 3;
   const int r = lane & 15, g = lane >> 4;
-  const int nk = N / KE;
+  const int nk = K / KE;
 
   // This wave's DMA share of a stage: group 0 -> A blocks 4q..4q+3 (16 rows
   // each, stored chunk-major), group 1 -> B blocks 4q..4q+3 (1 KiB each).
   // Wave-uniform 64-bit base + per-lane 32-bit offsets (saddr form).
-  const unsigned char *gbase = grp == 0 ? A + (int64_t)m0 * ld : B + (int64_t)n0 * ES;
-  const int64_t gstep = grp == 0 ? (int64_t)kFastKB : (int64_t)KE * ld;
+  const unsigned char *gbase = grp == 0 ? A + (int64_t)m0 * lda_b : B + (int64_t)n0 * ES;
+  const int64_t gstep = grp == 0 ? (int64_t)kFastKB : (int64_t)KE * ldb_b;
   unsigned voff[kDma];
 #pragma unroll
   for (int i = 0; i < kDma; ++i) {
     const int blk = q * 4 + i;
     if (grp == 0) {
-      voff[i] = (unsigned)((blk * 16 + (lane & 15)) * ld) + 16u * (lane >> 4);
+      voff[i] = (unsigned)((blk * 16 + (lane & 15)) * lda_b) + 16u * (lane >> 4);
     } else {
       int krow, c;
       if constexpr (!kI8) {
@@ -351,7 +355,7 @@ gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restr
         krow = blk * 4 + (lane >> 4);
         c = (lane & 15) ^ fb8_swz(krow);
       }
-      voff[i] = (unsigned)(krow * ld) + 16u * c;
+      voff[i] = (unsigned)(krow * ldb_b) + 16u * c;
     }
   }
   const unsigned lds0 = (grp == 0 ? lds_addr(sA) : lds_addr(sB)) + q * 4 * 1024;
@@ -469,29 +473,25 @@ gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restr
     for (int fm = 0; fm < FM; ++fm) {
       const int row = m0 + grp * 128 + fm * 16 + r;
       const int col = n0 + q * 64 + fn * 16 + 4 * g;
-      if constexpr (DT == TCU_BF16_BF16) {
-        const f32x4 v = acc[fn][fm];
-        *(u32x2 *)(C + ((int64_t)row * N + col) * 2) =
-            u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
-      } else {
-        *(u32x4 *)(C + ((int64_t)row * N + col) * 4) = bitcast<u32x4>(acc[fn][fm]);
-      }
+      store_out4<DT, true>(C + (int64_t)row * ldc_b + (int64_t)col * OB, acc[fn][fm], 4,
+                           accum != 0);
     }
   }
 }
 
-template <int DT, int BM, int BN, int WM, int WN>
-hipError_t launch_cfg(const void *A, const void *B, void *C, int64_t N, hipStream_t stream) {
-  const int tiles_m = (int)((N + BM - 1) / BM), tiles_n = (int)((N + BN - 1) / BN);
-  hipLaunchKernelGGL((gemm_kernel<DT, BM, BN, WM, WN>), dim3(tiles_m * tiles_n), dim3(64 * WM * WN),
-                     0, stream, (const unsigned char *)A, (const unsigned char *)B,
-                     (unsigned char *)C, (int)N, tiles_m, tiles_n);
+template <int DT, int BM, int BN, int WM, int WN, bool kVec>
+hipError_t launch_cfg(const RectArgs &a, hipStream_t stream) {
+  const int tiles_m = (int)((a.M + BM - 1) / BM), tiles_n = (int)((a.N + BN - 1) / BN);
+  hipLaunchKernelGGL((gemm_kernel<DT, BM, BN, WM, WN, kVec>), dim3(tiles_m * tiles_n),
+                     dim3(64 * WM * WN), 0, stream, (const unsigned char *)a.A,
+                     (const unsigned char *)a.B, (unsigned char *)a.C, (int)a.M, (int)a.N,
+                     (int)a.K, a.lda, a.ldb, a.ldc, a.accum ? 1 : 0, tiles_m, tiles_n);
   return hipGetLastError();
 }
 
-// Kernel selection: TCU_GEMM_KERNEL=fast forces the full-tile (ping-pong) kernel
-// wherever N % 256 == 0, =general forces the general kernel; unset or
-// =auto picks by size.
+// Kernel selection: TCU_GEMM_KERNEL=fast forces the full-tile (ping-pong)
+// kernel wherever its shape conditions hold, =general forces the general
+// kernel; unset or =auto picks by size.
 enum class GemmPath { kAuto, kFast, kGeneral };
 GemmPath gemm_path() {
   const char *v = std::getenv("TCU_GEMM_KERNEL");
@@ -502,34 +502,45 @@ GemmPath gemm_path() {
 }
 
 template <int DT>
-hipError_t launch_dt(const void *A, const void *B, void *C, int64_t N, hipStream_t stream,
-                     int num_cus) {
-  // The largest tiles that still give every CU a workgroup.
-  const int64_t big_tiles = ((N + 255) / 256) * ((N + 255) / 256);
+hipError_t launch_dt(const RectArgs &a, hipStream_t stream, int num_cus) {
+  constexpr int ES = in_bytes(DT), OB = out_bytes(DT);
+  constexpr int KE = kFastKB / ES;
+  const bool vec = (a.lda * ES) % 16 == 0 && (a.ldb * ES) % 16 == 0 && (a.ldc * OB) % 16 == 0;
+  const int64_t big_tiles = ((a.M + 255) / 256) * ((a.N + 255) / 256);
   const GemmPath path = gemm_path();
-  const bool fast_ok = (N % 256 == 0);
+  // The full-tile kernel: whole 256 x 256 tiles, whole K stages, and the
+  // per-lane 32-bit DMA offsets within a stage in range.
+  const bool fast_ok = vec && a.M % 256 == 0 && a.N % 256 == 0 && a.K % KE == 0 && a.K > 0 &&
+                       256 * a.lda * ES < ((int64_t)1 << 32) &&
+                       KE * a.ldb * ES < ((int64_t)1 << 32);
   if (fast_ok && (path == GemmPath::kFast || (path == GemmPath::kAuto && big_tiles >= num_cus))) {
-    const int t = (int)(N / 256);
-    hipLaunchKernelGGL((gemm_pp_kernel<DT, TCU_RING>), dim3(t * t), dim3(512), 0, stream,
-                       (const unsigned char *)A, (const unsigned char *)B, (unsigned char *)C,
-                       (int)N, t, t);
+    const int tm = (int)(a.M / 256), tn = (int)(a.N / 256);
+    hipLaunchKernelGGL((gemm_pp_kernel<DT, TCU_RING>), dim3(tm * tn), dim3(512), 0, stream,
+                       (const unsigned char *)a.A, (const unsigned char *)a.B,
+                       (unsigned char *)a.C, (int)a.K, a.lda, a.ldb, a.ldc, a.accum ? 1 : 0,
+                       tm, tn);
     return hipGetLastError();
   }
-  if (big_tiles >= num_cus) return launch_cfg<DT, 256, 256, 2, 2>(A, B, C, N, stream);
-  const int64_t mid_tiles = ((N + 127) / 128) * ((N + 127) / 128);
-  if (mid_tiles >= num_cus) return launch_cfg<DT, 128, 128, 2, 2>(A, B, C, N, stream);
-  return launch_cfg<DT, 64, 64, 2, 2>(A, B, C, N, stream);
+  // Element-wise operand access (pitches not multiples of 16 bytes).
+  if (!vec) return launch_cfg<DT, 64, 64, 2, 2, false>(a, stream);
+  // Otherwise the largest tiles that still give every CU a workgroup.
+  if (big_tiles >= num_cus) return launch_cfg<DT, 256, 256, 2, 2, true>(a, stream);
+  const int64_t mid_tiles = ((a.M + 127) / 128) * ((a.N + 127) / 128);
+  if (mid_tiles >= num_cus) return launch_cfg<DT, 128, 128, 2, 2, true>(a, stream);
+  return launch_cfg<DT, 64, 64, 2, 2, true>(a, stream);
 }
 
 }  // namespace
 
-hipError_t launch_gemm(int dtype, const void *A, const void *B, void *C, int64_t N,
-                       hipStream_t stream, int num_cus) {
+hipError_t launch_rect(int dtype, int s, const RectArgs &a, hipStream_t stream, int num_cus) {
+  // A single contiguous strip times a single block is one native call.
+  if (a.K == s && a.N == s && a.lda == s && a.ldb == s && a.ldc == s)
+    return launch_tall(dtype, s, a.A, a.M, a.B, a.C, a.accum, stream, num_cus);
   switch (dtype) {
-    case TCU_F16_F32: return launch_dt<TCU_F16_F32>(A, B, C, N, stream, num_cus);
-    case TCU_BF16_F32: return launch_dt<TCU_BF16_F32>(A, B, C, N, stream, num_cus);
-    case TCU_BF16_BF16: return launch_dt<TCU_BF16_BF16>(A, B, C, N, stream, num_cus);
-    case TCU_I8_I32: return launch_dt<TCU_I8_I32>(A, B, C, N, stream, num_cus);
+    case TCU_F16_F32: return launch_dt<TCU_F16_F32>(a, stream, num_cus);
+    case TCU_BF16_F32: return launch_dt<TCU_BF16_F32>(a, stream, num_cus);
+    case TCU_BF16_BF16: return launch_dt<TCU_BF16_BF16>(a, stream, num_cus);
+    case TCU_I8_I32: return launch_dt<TCU_I8_I32>(a, stream, num_cus);
   }
   return hipErrorInvalidValue;
 }

@@ -7,12 +7,24 @@
 
 namespace tcu {
 
-// Native call: C (n x s) = A (n x s) * B (s x s) for s in {16, 32}.
+// Native call: C (n x s) = A (n x s) * B (s x s) [+ C when accum], for s in
+// {16, 32}, contiguous operands.
 hipError_t launch_tall(int dtype, int s, const void *A, int64_t n, const void *B, void *C,
-                       hipStream_t stream, int num_cus);
+                       bool accum, hipStream_t stream, int num_cus);
 
-// Blocked product of Theorem 2 fused into one launch: C (N x N) = A * B.
-hipError_t launch_gemm(int dtype, const void *A, const void *B, void *C, int64_t N,
-                       hipStream_t stream, int num_cus);
+// C (M x N) = A (M x K) * B (K x N) [+ C when accum] with row pitches in
+// elements; 0 <= M, K, N <= 2^30, M and N positive.  Theorem 2's strips and
+// blocks fused into one launch (the square product is M = K = N).
+struct RectArgs {
+  const void *A;
+  int64_t lda;
+  const void *B;
+  int64_t ldb;
+  void *C;
+  int64_t ldc;
+  int64_t M, K, N;
+  bool accum;
+};
+hipError_t launch_rect(int dtype, int s, const RectArgs &args, hipStream_t stream, int num_cus);
 
 }  // namespace tcu

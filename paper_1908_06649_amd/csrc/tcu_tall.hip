@@ -35,7 +35,33 @@ constexpr int kTallThreads = 256;  // 4 waves per workgroup
 // with the 8 consecutive output columns 8g .. 8g+7.
 __device__ __forceinline__ int col32(int m, int h) { return 8 * (m >> 2) + 4 * h + (m & 3); }
 
-template <int DT, int S, int U>
+// 32-bit outputs: add the stored values (accumulating form, int32 with
+// two's-complement wrap-around) to the fresh block d, as raw words.
+template <int DT, typename Acc>
+__device__ __forceinline__ u32x4 add_stored(Acc d, const u32x4 *p) {
+  const u32x4 o = __builtin_nontemporal_load(p);
+  if constexpr (DT == TCU_I8_I32)
+    return bitcast<u32x4>(d) + o;
+  else
+    return bitcast<u32x4>(d + bitcast<f32x4>(o));
+}
+
+// bfloat16 outputs: 2*W values, the pairs (v[2i], v[2i+1]) packed per word,
+// with the stored values added first when accumulating.
+template <int W>
+__device__ __forceinline__ void pack_out(const float *v, unsigned *words, const unsigned *old) {
+#pragma unroll
+  for (int i = 0; i < W; ++i) {
+    float lo = v[2 * i], hi = v[2 * i + 1];
+    if (old) {
+      lo += bf16_to_f32(old[i] & 0xffffu);
+      hi += bf16_to_f32(old[i] >> 16);
+    }
+    words[i] = pack_bf16x2(lo, hi);
+  }
+}
+
+template <int DT, int S, int U, bool kAcc>
 __global__ __launch_bounds__(kTallThreads) void tall_kernel(const unsigned char *__restrict__ A,
                                                             int64_t n,
                                                             const unsigned char *__restrict__ B,
@@ -110,8 +136,10 @@ __global__ __launch_bounds__(kTallThreads) void tall_kernel(const unsigned char 
         for (int h = 0; h < kBlocks; ++h) d[h] = mfma_i8_k32(w[h], x[u], i32x4{0, 0, 0, 0});
         if (ok[u]) {
 #pragma unroll
-          for (int h = 0; h < kBlocks; ++h)
-            __builtin_nontemporal_store(bitcast<u32x4>(d[h]), (u32x4 *)(crow + (S == 32 ? 32 * g + 16 * h : 16 * g)));
+          for (int h = 0; h < kBlocks; ++h) {
+            u32x4 *p = (u32x4 *)(crow + (S == 32 ? 32 * g + 16 * h : 16 * g));
+            __builtin_nontemporal_store(kAcc ? add_stored<DT>(d[h], p) : bitcast<u32x4>(d[h]), p);
+          }
         }
       } else {
         f32x4 d[kBlocks];
@@ -124,18 +152,38 @@ __global__ __launch_bounds__(kTallThreads) void tall_kernel(const unsigned char 
         }
         if (ok[u]) {
           if constexpr (DT == TCU_BF16_BF16) {
+            // Output columns 4*kBlocks*g .. +4*kBlocks-1 of the row, in order.
+            float v[4 * kBlocks];
+#pragma unroll
+            for (int h = 0; h < kBlocks; ++h)
+#pragma unroll
+              for (int i = 0; i < 4; ++i) v[4 * h + i] = d[h][i];
             if constexpr (S == 32) {
-              u32x4 o = {pack_bf16x2(d[0][0], d[0][1]), pack_bf16x2(d[0][2], d[0][3]),
-                         pack_bf16x2(d[1][0], d[1][1]), pack_bf16x2(d[1][2], d[1][3])};
-              __builtin_nontemporal_store(o, (u32x4 *)(crow + 16 * g));
+              u32x4 *p = (u32x4 *)(crow + 16 * g);
+              unsigned w[4], old[4];
+              if (kAcc) {
+                const u32x4 o = __builtin_nontemporal_load(p);
+                for (int i = 0; i < 4; ++i) old[i] = o[i];
+              }
+              pack_out<4>(v, w, kAcc ? old : nullptr);
+              __builtin_nontemporal_store(u32x4{w[0], w[1], w[2], w[3]}, p);
             } else {
-              u32x2 o = {pack_bf16x2(d[0][0], d[0][1]), pack_bf16x2(d[0][2], d[0][3])};
-              __builtin_nontemporal_store(o, (u32x2 *)(crow + 8 * g));
+              u32x2 *p = (u32x2 *)(crow + 8 * g);
+              unsigned w[2], old[2];
+              if (kAcc) {
+                const u32x2 o = __builtin_nontemporal_load(p);
+                old[0] = o[0];
+                old[1] = o[1];
+              }
+              pack_out<2>(v, w, kAcc ? old : nullptr);
+              __builtin_nontemporal_store(u32x2{w[0], w[1]}, p);
             }
           } else {
 #pragma unroll
-            for (int h = 0; h < kBlocks; ++h)
-              __builtin_nontemporal_store(bitcast<u32x4>(d[h]), (u32x4 *)(crow + (S == 32 ? 32 * g + 16 * h : 16 * g)));
+            for (int h = 0; h < kBlocks; ++h) {
+              u32x4 *p = (u32x4 *)(crow + (S == 32 ? 32 * g + 16 * h : 16 * g));
+              __builtin_nontemporal_store(kAcc ? add_stored<DT>(d[h], p) : bitcast<u32x4>(d[h]), p);
+            }
           }
         }
       }
@@ -144,32 +192,37 @@ __global__ __launch_bounds__(kTallThreads) void tall_kernel(const unsigned char 
 }
 
 template <int DT, int S>
-hipError_t launch_one(const void *A, int64_t n, const void *B, void *C, hipStream_t stream,
-                      int num_cus) {
+hipError_t launch_one(const void *A, int64_t n, const void *B, void *C, bool accum,
+                      hipStream_t stream, int num_cus) {
   constexpr int U = 4;
   const int64_t ntiles = (n + 15) / 16;
   const int64_t want = (ntiles + 4 * U - 1) / (4 * U);
   const int64_t cap = (int64_t)num_cus * 16;
   const int blocks = (int)(want < cap ? want : cap);
-  hipLaunchKernelGGL((tall_kernel<DT, S, U>), dim3(blocks), dim3(kTallThreads), 0, stream,
-                     (const unsigned char *)A, n, (const unsigned char *)B, (unsigned char *)C,
-                     ntiles);
+  if (accum)
+    hipLaunchKernelGGL((tall_kernel<DT, S, U, true>), dim3(blocks), dim3(kTallThreads), 0,
+                       stream, (const unsigned char *)A, n, (const unsigned char *)B,
+                       (unsigned char *)C, ntiles);
+  else
+    hipLaunchKernelGGL((tall_kernel<DT, S, U, false>), dim3(blocks), dim3(kTallThreads), 0,
+                       stream, (const unsigned char *)A, n, (const unsigned char *)B,
+                       (unsigned char *)C, ntiles);
   return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_tall(int dtype, int s, const void *A, int64_t n, const void *B, void *C,
-                       hipStream_t stream, int num_cus) {
+                       bool accum, hipStream_t stream, int num_cus) {
   switch (dtype * 2 + (s == 32 ? 1 : 0)) {
-    case TCU_F16_F32 * 2 + 0: return launch_one<TCU_F16_F32, 16>(A, n, B, C, stream, num_cus);
-    case TCU_F16_F32 * 2 + 1: return launch_one<TCU_F16_F32, 32>(A, n, B, C, stream, num_cus);
-    case TCU_BF16_F32 * 2 + 0: return launch_one<TCU_BF16_F32, 16>(A, n, B, C, stream, num_cus);
-    case TCU_BF16_F32 * 2 + 1: return launch_one<TCU_BF16_F32, 32>(A, n, B, C, stream, num_cus);
-    case TCU_BF16_BF16 * 2 + 0: return launch_one<TCU_BF16_BF16, 16>(A, n, B, C, stream, num_cus);
-    case TCU_BF16_BF16 * 2 + 1: return launch_one<TCU_BF16_BF16, 32>(A, n, B, C, stream, num_cus);
-    case TCU_I8_I32 * 2 + 0: return launch_one<TCU_I8_I32, 16>(A, n, B, C, stream, num_cus);
-    case TCU_I8_I32 * 2 + 1: return launch_one<TCU_I8_I32, 32>(A, n, B, C, stream, num_cus);
+    case TCU_F16_F32 * 2 + 0: return launch_one<TCU_F16_F32, 16>(A, n, B, C, accum, stream, num_cus);
+    case TCU_F16_F32 * 2 + 1: return launch_one<TCU_F16_F32, 32>(A, n, B, C, accum, stream, num_cus);
+    case TCU_BF16_F32 * 2 + 0: return launch_one<TCU_BF16_F32, 16>(A, n, B, C, accum, stream, num_cus);
+    case TCU_BF16_F32 * 2 + 1: return launch_one<TCU_BF16_F32, 32>(A, n, B, C, accum, stream, num_cus);
+    case TCU_BF16_BF16 * 2 + 0: return launch_one<TCU_BF16_BF16, 16>(A, n, B, C, accum, stream, num_cus);
+    case TCU_BF16_BF16 * 2 + 1: return launch_one<TCU_BF16_BF16, 32>(A, n, B, C, accum, stream, num_cus);
+    case TCU_I8_I32 * 2 + 0: return launch_one<TCU_I8_I32, 16>(A, n, B, C, accum, stream, num_cus);
+    case TCU_I8_I32 * 2 + 1: return launch_one<TCU_I8_I32, 32>(A, n, B, C, accum, stream, num_cus);
   }
   return hipErrorInvalidValue;
 }

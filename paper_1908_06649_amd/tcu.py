@@ -7,6 +7,9 @@ fallback: if ``libtcu.so`` is missing or fails to load, every call raises.
 
     tcu_mm_tall(A, n, s, B, C)   C (n x s) = A (n x s) @ B (s x s)     (native call)
     tcu_gemm(A, B, C, N)         C (N x N) = A @ B, unit size tcu_get_unit()
+    tcu_gemm_rect(A, lda, B, ldb, C, ldc, M, K, N, flags)
+                                 C (M x N) = [C +] A (M x K) @ B (K x N); A, B and C
+                                 may be row-strided 2-D views (row pitch = ld)
 
 The element types are taken from the tensors: (float16 -> float32),
 (bfloat16 -> float32), (bfloat16 -> bfloat16) or (int8 -> int32).  Calls are
@@ -34,6 +37,9 @@ TCU_BF16_F32 = 1
 TCU_BF16_BF16 = 2
 TCU_I8_I32 = 3
 
+TCU_ACCUMULATE = 1
+TCU_MAX_RECT_DIM = 1 << 30
+
 # Every symbol include/tcu.h declares: name -> (restype, argtypes)
 _i64, _int, _vp = ctypes.c_int64, ctypes.c_int, ctypes.c_void_p
 SIGNATURES = {
@@ -47,6 +53,9 @@ SIGNATURES = {
     "tcu_gemm": (_int, [_vp, _vp, _vp, _i64]),
     "tcu_mm_tall_ex": (_int, [_vp, _i64, _int, _vp, _vp, _int, _vp]),
     "tcu_gemm_ex": (_int, [_vp, _vp, _vp, _i64, _int, _int, _vp]),
+    "tcu_gemm_rect": (_int, [_vp, _i64, _vp, _i64, _vp, _i64, _i64, _i64, _i64, _int]),
+    "tcu_gemm_rect_ex": (_int, [_vp, _i64, _vp, _i64, _vp, _i64, _i64, _i64, _i64, _int,
+                                _int, _int, _vp]),
     "tcu_calls": (_i64, []),
     "tcu_square_calls": (_i64, []),
     "tcu_work": (_i64, []),
@@ -180,6 +189,50 @@ def tcu_gemm_ex(A, B, C, N: int, s: int, stream_ptr: int | None = None) -> None:
     dev, (pa, pb, pc) = _marshal("tcu_gemm_ex", (A, B, C), (N * N, N * N, N * N))
     st = _stream_ptr(dev) if stream_ptr is None else stream_ptr
     _check(lib().tcu_gemm_ex(pa, pb, pc, int(N), int(s), dt, st), "tcu_gemm_ex")
+
+
+def _marshal_views(where: str, views):
+    """(tensor, rows, cols, ld) per operand: check that each is a 2-D view of
+    that shape with unit column stride and row pitch ld on one HIP device;
+    return the device and the view base pointers."""
+    dev = views[0][0].device
+    ptrs = []
+    for t, rows, cols, ld in views:
+        if t.device != dev or t.device.type != "cuda":
+            raise ValueError(f"{where}: all matrices must be on the same HIP device")
+        if t.dim() != 2 or tuple(t.shape) != (rows, cols):
+            raise ValueError(f"{where}: expected a {rows} x {cols} view, got {tuple(t.shape)}")
+        if cols > 1 and t.stride(1) != 1:
+            raise ValueError(f"{where}: rows must be contiguous (column stride 1)")
+        if rows > 1 and t.stride(0) != ld:
+            raise ValueError(f"{where}: row pitch {t.stride(0)} does not match ld={ld}")
+        ptrs.append(t.data_ptr())
+    return dev, ptrs
+
+
+def tcu_gemm_rect(A, lda: int, B, ldb: int, C, ldc: int, M: int, K: int, N: int,
+                  flags: int = 0) -> None:
+    """C (M x N) = A (M x K) @ B (K x N), or C += A @ B with flags=TCU_ACCUMULATE
+    (Corollary 1 / the D functions' update); unit size tcu_get_unit()."""
+    dt = _dtype_code(A.dtype, C.dtype)
+    dev, (pa, pb, pc) = _marshal_views(
+        "tcu_gemm_rect", ((A, M, K, lda), (B, K, N, ldb), (C, M, N, ldc)))
+    L = lib()
+    _check(L.tcu_set_dtype(dt), "tcu_gemm_rect")
+    _check(L.tcu_set_stream(_stream_ptr(dev)), "tcu_gemm_rect")
+    _check(L.tcu_gemm_rect(pa, int(lda), pb, int(ldb), pc, int(ldc), int(M), int(K), int(N),
+                           int(flags)), "tcu_gemm_rect")
+
+
+def tcu_gemm_rect_ex(A, lda: int, B, ldb: int, C, ldc: int, M: int, K: int, N: int, flags: int,
+                     s: int, stream_ptr: int | None = None) -> None:
+    """Stateless rectangular / accumulating product (unit size, dtype, stream as arguments)."""
+    dt = _dtype_code(A.dtype, C.dtype)
+    dev, (pa, pb, pc) = _marshal_views(
+        "tcu_gemm_rect_ex", ((A, M, K, lda), (B, K, N, ldb), (C, M, N, ldc)))
+    st = _stream_ptr(dev) if stream_ptr is None else stream_ptr
+    _check(lib().tcu_gemm_rect_ex(pa, int(lda), pb, int(ldb), pc, int(ldc), int(M), int(K),
+                                  int(N), int(flags), int(s), dt, st), "tcu_gemm_rect_ex")
 
 
 # --------------------------------------------------------- cost accounting

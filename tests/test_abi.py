@@ -185,3 +185,120 @@ def test_python_binding_marshalling_errors():
         tcu.tcu_mm_tall(A, 64, 16, B, C)
     with pytest.raises(tcu.TcuError):        # unsupported dtype pair
         tcu.tcu_mm_tall(A, 64, 16, B, C.to(torch.float16))
+
+
+# ------------------------------------------------ rectangular / accumulate
+NO_DEV = torch.cuda.device_count() == 0
+
+RECT_ERRORS = [
+    # (A, lda, B, ldb, C, ldc, M, K, N, flags, s, dtype) -> status
+    ((0, 64, PB, 64, PC, 64, 64, 64, 64, 0, 16, 0), tcu.TCU_ERR_NULL),
+    ((PA, 64, PB, 64, 0, 64, 64, 64, 64, 0, 16, 0), tcu.TCU_ERR_NULL),
+    ((PA, 64, PB, 64, PC, 64, 64, 64, 64, 2, 16, 0), tcu.TCU_ERR_UNSUPPORTED),   # unknown flag
+    ((PA, 64, PB, 64, PC, 64, 64, 64, 64, 0, 8, 0), tcu.TCU_ERR_UNSUPPORTED),
+    ((PA, 64, PB, 64, PC, 64, 64, 64, 64, 0, 16, 7), tcu.TCU_ERR_UNSUPPORTED),
+    ((PA, 64, PB, 64, PC, 64, -1, 64, 64, 0, 16, 0), tcu.TCU_ERR_SHAPE),
+    ((PA, 64, PB, 64, PC, 64, 64, -1, 64, 0, 16, 0), tcu.TCU_ERR_SHAPE),
+    ((PA, 1 << 31, PB, 64, PC, 64, 2, (1 << 30) + 1, 64, 0, 16, 0), tcu.TCU_ERR_SHAPE),
+    ((PA, 1 << 17, PB, 64, PC, 64, 64, 1 << 17, 64, 0, 32, 3), tcu.TCU_ERR_SHAPE),  # int8 K
+    ((PA, 63, PB, 64, PC, 64, 64, 64, 64, 0, 16, 0), tcu.TCU_ERR_SHAPE),        # lda < K
+    ((PA, 64, PB, 63, PC, 64, 64, 64, 64, 0, 16, 0), tcu.TCU_ERR_SHAPE),        # ldb < N
+    ((PA, 64, PB, 64, PC, 63, 64, 64, 64, 0, 16, 0), tcu.TCU_ERR_SHAPE),        # ldc < N
+    ((PA, 1 << 40, PB, 64, PC, 64, 2, 64, 64, 0, 16, 0), tcu.TCU_ERR_SHAPE),    # pitch too big
+    ((PA, 1 << 30, PB, 64, PC, 64, 1024, 64, 64, 0, 16, 0), tcu.TCU_ERR_SHAPE),  # extent 2^41 B
+    ((PA + 2, 64, PB, 64, PC, 64, 64, 64, 64, 0, 16, 0), tcu.TCU_ERR_ALIGN),
+    ((PA, 64, PB, 64, PC + 8, 64, 64, 64, 64, 0, 16, 0), tcu.TCU_ERR_ALIGN),
+    # C is A (same block)
+    ((PA, 64, PB, 64, PA, 64, 64, 64, 64, 0, 16, 2), tcu.TCU_ERR_OVERLAP),
+    # C = columns 32..95 of a 1024-wide bf16 array, A = columns 0..63: shared columns
+    ((PA, 1024, PB, 64, PA + 64, 1024, 64, 64, 64, 0, 16, 2), tcu.TCU_ERR_OVERLAP),
+    # C's rows start 64 bytes before the end of A's grid rows and wrap into row 1
+    ((PA, 1024, PB, 64, PA + 2048 - 64, 1024, 64, 64, 64, 0, 16, 2), tcu.TCU_ERR_OVERLAP),
+    # different byte pitches over the same range: reported conservatively
+    ((PA, 1024, PB, 64, PA + 1024, 512, 64, 64, 64, 0, 16, 2), tcu.TCU_ERR_OVERLAP),
+    # C overlaps B
+    ((PA, 64, PB, 64, PB + 64 * 128 - 16, 64, 64, 64, 64, 1, 16, 2), tcu.TCU_ERR_OVERLAP),
+]
+
+
+@pytest.mark.parametrize("args,want", RECT_ERRORS)
+def test_rect_rejects(L, args, want):
+    L.tcu_reset_calls()
+    assert L.tcu_gemm_rect_ex(*args, None) == want
+    assert L.tcu_calls() == 0 and L.tcu_work() == 0
+
+
+def test_rect_empty_is_a_noop(L):
+    """M = 0, N = 0, or K = 0 when accumulating: success with no device work
+    and no calls (fake pointers are never touched)."""
+    L.tcu_reset_calls()
+    assert L.tcu_gemm_rect_ex(PA, 64, PB, 64, PC, 64, 0, 64, 64, 0, 16, 0, None) == tcu.TCU_OK
+    assert L.tcu_gemm_rect_ex(PA, 64, PB, 64, PC, 64, 64, 64, 0, 1, 16, 0, None) == tcu.TCU_OK
+    assert L.tcu_gemm_rect_ex(PA, 64, PB, 64, PC, 64, 64, 0, 64, 1, 32, 3, None) == tcu.TCU_OK
+    # operands without elements may be NULL
+    assert L.tcu_gemm_rect_ex(None, 0, None, 64, PC, 64, 64, 0, 64, 1, 16, 0, None) == tcu.TCU_OK
+    assert L.tcu_gemm_rect_ex(None, 64, PB, 64, None, 64, 0, 64, 64, 0, 16, 0, None) == tcu.TCU_OK
+    assert L.tcu_gemm_rect_ex(PA, 64, None, 0, None, 0, 64, 64, 0, 0, 16, 0, None) == tcu.TCU_OK
+    assert L.tcu_gemm_rect_ex(None, 0, None, 64, None, 64, 64, 0, 64, 1, 16, 0, None) \
+        == tcu.TCU_ERR_NULL
+    assert L.tcu_calls() == 0 and L.tcu_square_calls() == 0 and L.tcu_work() == 0
+
+
+@pytest.mark.skipif(not NO_DEV, reason="a HIP device is visible (valid calls would launch)")
+def test_rect_disjoint_blocks_of_one_array_pass(L):
+    """The D functions update one block of an array from two others: with one
+    byte pitch the check is element-exact, so disjoint blocks are accepted."""
+    P = 1024 * 2      # bytes per row of a 1024-wide bfloat16 array at PA
+    blk = lambda r, c: PA + r * P + c * 2
+    # X = block (0, 64), Y = block (0, 0), Z = block (64, 64), all 64 x 64
+    rc = L.tcu_gemm_rect_ex(blk(0, 0), 1024, blk(64, 64), 1024, blk(0, 64), 1024,
+                            64, 64, 64, tcu.TCU_ACCUMULATE, 16, tcu.TCU_BF16_BF16, None)
+    assert rc == tcu.TCU_ERR_NO_DEVICE
+    # X right next to Y in the same rows, and X = the block just below Y
+    assert L.tcu_gemm_rect_ex(blk(0, 0), 1024, blk(64, 0), 1024, blk(0, 64), 1024,
+                              64, 64, 64, 1, 16, 2, None) == tcu.TCU_ERR_NO_DEVICE
+    assert L.tcu_gemm_rect_ex(blk(0, 0), 1024, blk(0, 64), 1024, blk(64, 0), 1024,
+                              64, 64, 64, 1, 16, 2, None) == tcu.TCU_ERR_NO_DEVICE
+
+
+def _brute_overlap(a, ar, aw, ap, b, br, bw, bp):
+    """Do two row-major byte views share a byte?  (set intersection)"""
+    sa = {a + i * ap + j for i in range(ar) for j in range(aw)}
+    return any(b + i * bp + j in sa for i in range(br) for j in range(bw))
+
+
+@pytest.mark.skipif(not NO_DEV, reason="a HIP device is visible (valid calls would launch)")
+def test_rect_overlap_check_vs_brute_force(L):
+    """The element-exact overlap test against set intersection on small
+    random views of one bfloat16 array (2-byte elements in and out): exact
+    when the pitches agree, never missing a real overlap otherwise."""
+    import random
+    rng = random.Random(5)
+    n_same = n_hit = 0
+    for _ in range(3000):
+        M, K, N = rng.randint(1, 4), rng.randint(1, 24), rng.randint(1, 24)
+        lda = K + 8 * rng.randint(0, 3)
+        ldc = lda if rng.random() < 0.7 else N + 8 * rng.randint(0, 3)
+        ldc = max(ldc, N)
+        offa = 16 * rng.randint(0, 40)
+        offc = 16 * rng.randint(0, 40)
+        A, C = PA + offa, PA + offc
+        rc = L.tcu_gemm_rect_ex(A, lda, PB, N, C, ldc, M, K, N, 0, 16, tcu.TCU_BF16_BF16, None)
+        real = _brute_overlap(C, M, 2 * N, 2 * ldc, A, M, 2 * K, 2 * lda)
+        if real:
+            n_hit += 1
+            assert rc == tcu.TCU_ERR_OVERLAP
+        same_pitch = ldc == lda or M == 1
+        if same_pitch and not real:
+            assert rc == tcu.TCU_ERR_NO_DEVICE, (M, K, N, lda, ldc, offa, offc)
+        if same_pitch:
+            n_same += 1
+    assert n_same > 1000 and n_hit > 300
+
+
+def test_python_rect_marshalling_errors():
+    A = torch.zeros(64, 32, dtype=torch.bfloat16)
+    B = torch.zeros(32, 16, dtype=torch.bfloat16)
+    C = torch.zeros(64, 16, dtype=torch.float32)
+    with pytest.raises(ValueError):          # host tensors
+        tcu.tcu_gemm_rect(A, 32, B, 16, C, 16, 64, 32, 16)
