@@ -16,9 +16,17 @@ JSON line:
   secondary  the other workloads measured the same way: the very tall
              bf16 native call (GB/s vs HBM peak), the int8 product (TOP/s),
              the 4096 x 16 native call and the N = 1024 fp16 product
+  rect       the rectangular / accumulating product (tcu_gemm_rect):
+             Corollary 1's sqrt(n) x r by r x sqrt(n) with r below and above
+             sqrt(n), accumulating into C, and an order-8200 product that
+             needs zero padding (TFLOP/s or TOP/s vs matrix-core peak)
   cost_model calls issued vs Theorem 2's count and bound, weak-model square
              calls, model work, and the per-call latency l fitted as the
              intercept of t(n) = a*n + l for native calls
+
+Timing: every measured call first runs back to back, untimed, for 0.3 s
+(the GPU leaves its idle clock state), then W untimed warmup calls, then K
+calls bracketed by HIP events on the stream the library launches on.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
        [--no-cpu-baseline] [--no-secondary] [--copy-probe]
@@ -48,7 +56,7 @@ PROFILES = os.path.join(ROOT, "profiles")
 
 
 def kernel_sources(kind: str):
-    main = "tcu_gemm.hip" if kind == "gemm" else "tcu_tall.hip"
+    main = "tcu_gemm.hip" if kind in ("gemm", "rect") else "tcu_tall.hip"
     return [os.path.join(CSRC, f) for f in (main, "tcu_device.h")]
 
 
@@ -88,8 +96,12 @@ def algorithmic(spec: dict):
     if spec["kind"] == "tall":
         n, s = spec["n"], spec["s"]
         return 2.0 * n * s * s, n * s * ib + s * s * ib + n * s * ob
-    N = spec["N"]
     del inputs
+    if spec["kind"] == "rect":
+        M, K, N = spec["M"], spec["K"], spec["N"]
+        c_io = 2 if spec.get("acc") else 1          # C read too when accumulating
+        return 2.0 * M * K * N, (M * K + K * N) * ib + c_io * M * N * ob
+    N = spec["N"]
     return 2.0 * N ** 3, 2 * N * N * ib + N * N * ob
 
 
@@ -99,26 +111,52 @@ class Workload:
     def __init__(self, name: str):
         import torch
         from paper_1908_06649_amd import inputs, tcu
-        self.name, self.spec = name, inputs.WORKLOADS[name]
+        self.name = name
+        self.spec = inputs.WORKLOADS.get(name) or inputs.RECT_WORKLOADS[name]
         self.tcu = tcu
         self.A, self.B = inputs.make_inputs(self.spec)
         self.dA, self.dB = self.A.cuda(), self.B.cuda()
         _, _, c_shape = inputs.shapes(self.spec)
-        self.C = torch.empty(c_shape, dtype=inputs.TORCH_DTYPE[self.spec["out"]], device="cuda")
+        if self.spec.get("acc"):
+            self.C = inputs.make_c0(self.spec).cuda()
+        else:
+            self.C = torch.empty(c_shape, dtype=inputs.TORCH_DTYPE[self.spec["out"]],
+                                 device="cuda")
         self.s = self.spec["s"]
 
     def call(self):
         sp = self.spec
         if sp["kind"] == "gemm":
             self.tcu.tcu_gemm(self.dA, self.dB, self.C, sp["N"])
+        elif sp["kind"] == "rect":
+            M, K, N = sp["M"], sp["K"], sp["N"]
+            self.tcu.tcu_gemm_rect(self.dA, K, self.dB, N, self.C, N, M, K, N,
+                                   self.tcu.TCU_ACCUMULATE if sp["acc"] else 0)
         else:
             self.tcu.tcu_mm_tall(self.dA, sp["n"], sp["s"], self.dB, self.C)
 
 
+SETTLE_S = 0.3
+
+
+def settle(fn, seconds: float = SETTLE_S) -> None:
+    """Run the call back to back for `seconds` (untimed) so the GPU leaves
+    its idle clock state: after the host-side input generation the device has
+    been idle, and the first milliseconds of work run measurably slower."""
+    import torch
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(8):
+            fn()
+        torch.cuda.synchronize()
+
+
 def time_steps(fn, steps: int, warmup: int) -> float:
     """Average ms per call over `steps` back-to-back calls, timed with HIP
-    events on the current stream (the stream the library launches on)."""
+    events on the current stream (the stream the library launches on),
+    after a clock-settling period and `warmup` untimed calls."""
     import torch
+    settle(fn)
     for _ in range(warmup):
         fn()
     torch.cuda.synchronize()
@@ -148,7 +186,7 @@ def measure(name: str, steps: int, warmup: int) -> dict:
     kind = sp["kind"]
     out = {"workload": name, "ms_per_call": ms, "calls": calls, "square_calls": squares,
            "model_work": work}
-    if kind == "gemm":
+    if kind in ("gemm", "rect"):
         tput = flops / (ms * 1e-3) / 1e12
         peak = PEAK[sp["dtype"]]
         out.update({"value": tput, "unit": "TOP/s" if sp["dtype"] == "i8" else "TFLOP/s",
@@ -156,8 +194,11 @@ def measure(name: str, steps: int, warmup: int) -> dict:
                                  "unit": "TOP/s" if sp["dtype"] == "i8" else "TFLOP/s",
                                  "frac": tput / peak,
                                  "traffic": counted_traffic(name, kind)},
-                    "calls_theorem2": (sp["N"] // sp["s"]) ** 2,
                     "algorithmic_flops": flops, "compulsory_bytes": nbytes})
+        if kind == "gemm":
+            out["calls_theorem2"] = (sp["N"] // sp["s"]) ** 2
+        else:   # Corollary 1 on the zero-padded operands
+            out["calls_corollary1"] = -(-sp["K"] // sp["s"]) * -(-sp["N"] // sp["s"])
     else:
         gbs = nbytes / (ms * 1e-3) / 1e9
         out.update({"value": gbs, "unit": "GB/s",
@@ -252,6 +293,7 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default=HEADLINE)
+    ap.add_argument("--no-rect", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--copy-probe", action="store_true")
@@ -271,9 +313,9 @@ def main() -> int:
     if args.copy_probe:
         copy_probe()
         return 0
-    if args.workload not in inputs.WORKLOADS:
-        print(f"unknown workload {args.workload}; choose from {sorted(inputs.WORKLOADS)}",
-              file=sys.stderr)
+    if args.workload not in inputs.WORKLOADS and args.workload not in inputs.RECT_WORKLOADS:
+        names = sorted(inputs.WORKLOADS) + sorted(inputs.RECT_WORKLOADS)
+        print(f"unknown workload {args.workload}; choose from {names}", file=sys.stderr)
         return 2
 
     main_res = measure(args.workload, args.steps, args.warmup)
@@ -293,7 +335,7 @@ def main() -> int:
         "dtype": sp["dtype"],
         "data": "synthetic (seeded i.i.d. matrices; the paper has no datasets)",
         "config": {"workload": args.workload,
-                   **{k: sp[k] for k in ("kind", "N", "n", "s") if k in sp},
+                   **{k: sp[k] for k in ("kind", "M", "K", "N", "n", "s", "acc") if k in sp},
                    "dtype_in": sp["dtype"], "dtype_out": sp["out"],
                    "distribution": sp["dist"], "seed": sp["seed"]},
         "roofline": main_res["roofline"],
@@ -301,6 +343,8 @@ def main() -> int:
     cost = {k: main_res[k] for k in ("calls", "square_calls", "model_work") if k in main_res}
     if sp["kind"] == "gemm":
         cost["calls_theorem2_and_lower_bound"] = main_res["calls_theorem2"]
+    elif sp["kind"] == "rect":
+        cost["calls_corollary1"] = main_res["calls_corollary1"]
     if not args.no_cpu_baseline and sp["kind"] == "gemm":
         result["cpu_baseline"] = cpu_baseline(w)
     else:
@@ -322,6 +366,17 @@ def main() -> int:
             torch.cuda.empty_cache()
         result["secondary"] = sec
         cost["ell_fit"] = ell_fit()
+    if not args.no_rect:
+        rect = {}
+        for name in inputs.RECT_WORKLOADS:
+            if name == args.workload:
+                continue
+            r = measure(name, args.steps, max(args.warmup, 5))
+            r.pop("_workload")
+            rect[name] = {k: r[k] for k in ("value", "unit", "ms_per_call", "roofline", "calls",
+                                            "calls_corollary1", "square_calls", "model_work")}
+            torch.cuda.empty_cache()
+        result["rect"] = rect
     result["cost_model"] = cost
     result["kernel_source_sha256"] = {"gemm": kernel_hash("gemm"), "tall": kernel_hash("tall")}
     print(json.dumps(result), flush=True)

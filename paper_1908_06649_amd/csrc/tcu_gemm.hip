@@ -122,7 +122,31 @@ gemm_kernel(const unsigned char *__restrict__ A, const unsigned char *__restrict
   u32x4 rb[CB][8];
 
   // ---- global -> registers for the K-step starting at element k0 ----
-  auto gload = [&](int k0) {
+  // Whole tile inside M x N: only the last K-step can reach past K, and
+  // only when K is not a multiple of the step.  Interior steps load whole
+  // chunks with no per-element checks.
+  const bool interior = kVec && m0 + BM <= M && n0 + BN <= N;
+  auto gload_full = [&](int k0) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < CA; ++i) {
+      const int q = tid + NT * i;
+      const int row = m0 + (q >> 3), kc = k0 + (q & 7) * EPC;
+      ra[i] = *(const u32x4 *)(A + (int64_t)row * lda_b + (int64_t)kc * ES);
+    }
+#pragma unroll
+    for (int i = 0; i < CB; ++i) {
+      const int q = tid + NT * i;
+      if (CB * NT > NBLK && q >= NBLK) break;
+      const int nb = q % NBW, kb = q / NBW;
+      const int nc = n0 + nb * EPC;
+#pragma unroll
+      for (int rr = 0; rr < 8; ++rr) {
+        const int k = k0 + 8 * kb + rr;
+        rb[i][rr] = *(const u32x4 *)(B + (int64_t)k * ldb_b + (int64_t)nc * ES);
+      }
+    }
+  };
+  auto gload_edge = [&](int k0) __attribute__((always_inline)) {
 #pragma unroll
     for (int i = 0; i < CA; ++i) {
       const int q = tid + NT * i;
@@ -143,6 +167,12 @@ gemm_kernel(const unsigned char *__restrict__ A, const unsigned char *__restrict
                                          k < K ? nvalid : 0);
       }
     }
+  };
+  auto gload = [&](int k0) __attribute__((always_inline)) {
+    if (interior && k0 + BK <= K)
+      gload_full(k0);
+    else
+      gload_edge(k0);
   };
 
   // ---- registers -> LDS buffer `buf` (B transposed on the way) ----
@@ -243,17 +273,21 @@ gemm_kernel(const unsigned char *__restrict__ A, const unsigned char *__restrict
     for (int fm = 0; fm < FM; ++fm) {
       const int row = m0 + wm * WTM + 16 * fm + r;
       const int col = n0 + wn * WTN + 16 * fn + 4 * g;
-      const int valid = row < M ? min(max(N - col, 0), 4) : 0;
-      if (valid > 0)
-        store_out4<DT, kVec>(C + (int64_t)row * ldc_b + (int64_t)col * OB, acc[fn][fm], valid,
-                             accum != 0);
+      unsigned char *p = C + (int64_t)row * ldc_b + (int64_t)col * OB;
+      if (interior) {
+        store_out4<DT, true>(p, acc[fn][fm], 4, accum != 0);
+      } else {
+        const int valid = row < M ? min(max(N - col, 0), 4) : 0;
+        if (valid > 0) store_out4<DT, kVec>(p, acc[fn][fm], valid, accum != 0);
+      }
     }
   }
 }
 
 // ---------------------------------------------------------------------------
-// Full-tile kernel (N a multiple of 256): 256 x 256 output tile per
-// workgroup and a ring of LDS stages, each holding 64 bytes of the
+// Full-tile kernel (M, N multiples of 256, K a multiple of one stage):
+// 256 x 256 output tiles, a persistent grid of one workgroup per CU walking
+// the tiles, and a ring of LDS stages, each holding 64 bytes of the
 // contracted index (32 16-bit or 64 int8 values: one matrix-core K step, and
 // one or two strips A_i of the unit).
 //   * Both operands go HBM/L2 -> LDS with direct 16-byte DMA loads
@@ -325,9 +359,16 @@ gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restr
   __shared__ __attribute__((aligned(1024))) unsigned char sA[kRing * kFastStage];
   __shared__ __attribute__((aligned(1024))) unsigned char sB[kRing * kFastStage];
 
-  int tm, tn;
-  map_tile(blockIdx.x, tiles_m, tiles_n, tm, tn);
-  const int m0 = tm * 256, n0 = tn * 256;
+  const int total = tiles_m * tiles_n;
+  int tile = blockIdx.x;
+  int m0, n0;
+  auto place = [&](int t) {
+    int tm, tn;
+    map_tile(t, tiles_m, tiles_n, tm, tn);
+    m0 = tm * 256;
+    n0 = tn * 256;
+  };
+  place(tile);
   const int64_t lda_b = lda * ES, ldb_b = ldb * ES, ldc_b = ldc * OB;
   const int lane = threadIdx.x & 63;
   const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -338,7 +379,9 @@ gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restr
   // This wave's DMA share of a stage: group 0 -> A blocks 4q..4q+3 (16 rows
   // each, stored chunk-major), group 1 -> B blocks 4q..4q+3 (1 KiB each).
   // Wave-uniform 64-bit base + per-lane 32-bit offsets (saddr form).
-  const unsigned char *gbase = grp == 0 ? A + (int64_t)m0 * lda_b : B + (int64_t)n0 * ES;
+  const unsigned char *gbase;
+  auto set_gbase = [&]() { gbase = grp == 0 ? A + (int64_t)m0 * lda_b : B + (int64_t)n0 * ES; };
+  set_gbase();
   const int64_t gstep = grp == 0 ? (int64_t)kFastKB : (int64_t)KE * ldb_b;
   unsigned voff[kDma];
 #pragma unroll
@@ -384,11 +427,6 @@ gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restr
   constexpr int kW1 = (kI8 ? 8 : 4) * BROW;
 
   Acc acc[FN][FM];
-#pragma unroll
-  for (int a = 0; a < FN; ++a)
-#pragma unroll
-    for (int b = 0; b < FM; ++b) acc[a][b] = Acc{0, 0, 0, 0};
-
   u32x4 xf[FM], wf[FN];
   auto read_frags = [&](int slot_) {
     const unsigned char *sa = sA + slot_ * kFastStage;
@@ -443,39 +481,55 @@ gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restr
 
   for (int s0 = 0; s0 < kRing; ++s0)
     if (s0 < nk) issue(s0, s0);
-  wait_stage(nk - 1 < kRing - 1 ? nk - 1 : kRing - 1);
-  int slot = 0;
-  if (grp == 0) {
-    read_frags(0);
-    for (int t = 0; t < nk; ++t) {
-      mfmas();                                            // A(t): compute stage t
-      wait_stage(later_after(t));
-      if (t + kRing < nk) issue(slot, t + kRing);         // B(t): refill, read t+1
-      if (t + 1 < nk) read_frags(next_slot(slot));
-      vm_wait_barrier<63>();
-      slot = next_slot(slot);
+  // Persistent loop over output tiles: after a tile's epilogue stores, the
+  // first stages of the next tile are issued at once, so their loads overlap
+  // the stores' drain instead of waiting for a new workgroup.
+  for (;;) {
+#pragma unroll
+    for (int a = 0; a < FN; ++a)
+#pragma unroll
+      for (int b = 0; b < FM; ++b) acc[a][b] = Acc{0, 0, 0, 0};
+    wait_stage(nk - 1 < kRing - 1 ? nk - 1 : kRing - 1);
+    int slot = 0;
+    if (grp == 0) {
+      read_frags(0);
+      for (int t = 0; t < nk; ++t) {
+        mfmas();                                            // A(t): compute stage t
+        wait_stage(later_after(t));
+        if (t + kRing < nk) issue(slot, t + kRing);         // B(t): refill, read t+1
+        if (t + 1 < nk) read_frags(next_slot(slot));
+        vm_wait_barrier<63>();
+        slot = next_slot(slot);
+      }
+    } else {
+      for (int t = 0; t < nk; ++t) {
+        if (t >= 1 && t - 1 + kRing < nk) issue(prev_slot(slot), t - 1 + kRing);
+        read_frags(slot);                                   // A(t): refill, read t
+        wait_stage(later_after(t));
+        mfmas();                                            // B(t): compute stage t
+        vm_wait_barrier<63>();
+        slot = next_slot(slot);
+      }
     }
-  } else {
-    for (int t = 0; t < nk; ++t) {
-      if (t >= 1 && t - 1 + kRing < nk) issue(prev_slot(slot), t - 1 + kRing);
-      read_frags(slot);                                   // A(t): refill, read t
-      wait_stage(later_after(t));
-      mfmas();                                            // B(t): compute stage t
-      vm_wait_barrier<63>();
-      slot = next_slot(slot);
-    }
-  }
 
-  // Epilogue: lane holds C[row][col .. col+3] of every accumulator block.
+    // Epilogue: lane holds C[row][col .. col+3] of every accumulator block.
 #pragma unroll
-  for (int fn = 0; fn < FN; ++fn) {
+    for (int fn = 0; fn < FN; ++fn) {
 #pragma unroll
-    for (int fm = 0; fm < FM; ++fm) {
-      const int row = m0 + grp * 128 + fm * 16 + r;
-      const int col = n0 + q * 64 + fn * 16 + 4 * g;
-      store_out4<DT, true>(C + (int64_t)row * ldc_b + (int64_t)col * OB, acc[fn][fm], 4,
-                           accum != 0);
+      for (int fm = 0; fm < FM; ++fm) {
+        const int row = m0 + grp * 128 + fm * 16 + r;
+        const int col = n0 + q * 64 + fn * 16 + 4 * g;
+        store_out4<DT, true>(C + (int64_t)row * ldc_b + (int64_t)col * OB, acc[fn][fm], 4,
+                             accum != 0);
+      }
     }
+    // Every wave finished reading the ring at the last barrier of the loop.
+    tile += gridDim.x;
+    if (tile >= total) break;
+    place(tile);
+    set_gbase();
+    for (int s0 = 0; s0 < kRing; ++s0)
+      if (s0 < nk) issue(s0, s0);
   }
 }
 
@@ -515,7 +569,14 @@ hipError_t launch_dt(const RectArgs &a, hipStream_t stream, int num_cus) {
                        KE * a.ldb * ES < ((int64_t)1 << 32);
   if (fast_ok && (path == GemmPath::kFast || (path == GemmPath::kAuto && big_tiles >= num_cus))) {
     const int tm = (int)(a.M / 256), tn = (int)(a.N / 256);
-    hipLaunchKernelGGL((gemm_pp_kernel<DT, TCU_RING>), dim3(tm * tn), dim3(512), 0, stream,
+    // Persistent grid: one workgroup per CU (the LDS ring admits one), each
+    // walking tiles blockIdx, blockIdx + grid, ...  TCU_PP_GRID=<g> sets the
+    // grid size instead (tests use a tiny grid to give every workgroup many
+    // tiles).
+    const char *gv = std::getenv("TCU_PP_GRID");
+    const int want = gv && std::atoi(gv) > 0 ? std::atoi(gv) : num_cus;
+    const int grid = want < tm * tn ? want : tm * tn;
+    hipLaunchKernelGGL((gemm_pp_kernel<DT, TCU_RING>), dim3(grid), dim3(512), 0, stream,
                        (const unsigned char *)a.A, (const unsigned char *)a.B,
                        (unsigned char *)a.C, (int)a.K, a.lda, a.ldb, a.ldc, a.accum ? 1 : 0,
                        tm, tn);

@@ -32,6 +32,22 @@ WORKLOADS = {
                                     s=32, dist="normal", seed=4),
 }
 
+# Workloads of the rectangular / accumulating product (tcu_gemm_rect):
+# C (M x N) [+]= A (M x K) * B (K x N).  Corollary 1's sqrt(n) x r times
+# r x sqrt(n) with r below and above sqrt(n), and a product whose order is
+# not a multiple of the unit (zero padding).  "acc": accumulate into a
+# seeded initial C.
+RECT_WORKLOADS = {
+    "cor1_bf16_M8192_K2048_N8192_acc": dict(kind="rect", dtype="bf16", out="f32", M=8192,
+                                            K=2048, N=8192, s=32, acc=True, dist="normal",
+                                            seed=5),
+    "cor1_i8_M2048_K65536_N2048_acc": dict(kind="rect", dtype="i8", out="i32", M=2048,
+                                           K=65536, N=2048, s=32, acc=True, dist="int8",
+                                           seed=6),
+    "pad_bf16_M8200_K8200_N8200": dict(kind="rect", dtype="bf16", out="bf16", M=8200, K=8200,
+                                       N=8200, s=32, acc=False, dist="normal", seed=7),
+}
+
 TORCH_DTYPE = {"f16": torch.float16, "bf16": torch.bfloat16, "i8": torch.int8,
                "f32": torch.float32, "i32": torch.int32}
 
@@ -58,6 +74,9 @@ def shapes(spec: dict):
     if spec["kind"] == "tall":
         n, s = spec["n"], spec["s"]
         return (n, s), (s, s), (n, s)
+    if spec["kind"] == "rect":
+        M, K, N = spec["M"], spec["K"], spec["N"]
+        return (M, K), (K, N), (M, N)
     N = spec["N"]
     return (N, N), (N, N), (N, N)
 
@@ -70,6 +89,18 @@ def make_inputs(spec: dict, seed: int | None = None):
     A = draw(a_shape, spec["dtype"], spec["dist"], gen)
     B = draw(b_shape, spec["dtype"], spec["dist"], gen)
     return A, B
+
+
+def make_c0(spec: dict) -> torch.Tensor:
+    """Initial output of an accumulating workload: standard normal in the
+    output type (float32 or bfloat16), or int32 uniform in [-2^20, 2^20),
+    from its own generator seeded with the workload's seed + 1000."""
+    gen = torch.Generator(device="cpu")
+    gen.manual_seed(spec["seed"] + 1000)
+    _, _, c_shape = shapes(spec)
+    if spec["out"] == "i32":
+        return torch.randint(-(1 << 20), 1 << 20, c_shape, generator=gen, dtype=torch.int32)
+    return torch.randn(c_shape, generator=gen, dtype=torch.float32).to(TORCH_DTYPE[spec["out"]])
 
 
 def small_ints(shape, dtype: str, seed: int) -> torch.Tensor:

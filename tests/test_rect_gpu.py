@@ -81,6 +81,16 @@ def test_rect_full_tiles(M, K, N, din, out, accumulate, kernel, monkeypatch):
     run_and_check(M, K, N, din, out, 32, "padded", accumulate, seed=M + K + N)
 
 
+@pytest.mark.parametrize("din,out", PAIRS)
+@pytest.mark.parametrize("accumulate", [False, True])
+def test_rect_full_tiles_many_per_workgroup(din, out, accumulate, monkeypatch):
+    """The full-tile kernel's persistent loop with 3 workgroups for 12 tiles
+    of 256 x 256 (each workgroup walks 4 tiles, reloading its ring)."""
+    monkeypatch.setenv("TCU_GEMM_KERNEL", "fast")
+    monkeypatch.setenv("TCU_PP_GRID", "3")
+    run_and_check(768, 512, 1024, din, out, 32, "padded", accumulate, seed=12)
+
+
 @pytest.mark.parametrize("s", [16, 32])
 @pytest.mark.parametrize("din,out", PAIRS)
 @pytest.mark.parametrize("M", [7, 16, 4099])
@@ -206,14 +216,18 @@ def test_rect_d_function_in_place_blocks(s):
 
 
 # Corollary 1 at full size, on sampled rows: sqrt(n) x r times r x sqrt(n)
-# with r below and above sqrt(n).
+# with r below and above sqrt(n), plus the benchmark's rectangular workloads
+# exactly as the benchmark runs them (contiguous operands).
 COR1 = [
     # (M = N = sqrt(n), K = r, in, out, accumulate)
-    (8192, 2048, "bf16", "f32", True),
     (8192, 1024, "i8", "i32", False),
-    (2048, 65536, "i8", "i32", True),
     (2048, 32768, "bf16", "bf16", True),
+    (4096, 4096 + 32, "f16", "f32", True),
 ]
+
+
+def sampled_rows(M, seed=1):
+    return np.unique(np.concatenate([[0, M - 1], np.random.default_rng(seed).integers(0, M, 30)]))
 
 
 @pytest.mark.parametrize("M,K,din,out,accumulate", COR1)
@@ -222,6 +236,19 @@ def test_rect_corollary1_sampled(M, K, din, out, accumulate):
     A, B = gu.draw_pair((M, K), (K, N), din, 5)
     C0 = gu.c0_draw((M, N), out, 6) if accumulate else None
     got = gu.run_rect(A, B, 32, din, out, K, N, N, C0=C0)
-    rows = np.unique(np.concatenate([[0, M - 1], np.random.default_rng(1).integers(0, M, 30)]))
+    rows = sampled_rows(M)
     compare.check(din, out, inputs.bits(A), inputs.bits(B), got[rows], rows=rows,
                   C0=None if C0 is None else to_np_c0(C0, out))
+
+
+@pytest.mark.parametrize("name", sorted(inputs.RECT_WORKLOADS))
+def test_rect_workload_sampled(name):
+    sp = inputs.RECT_WORKLOADS[name]
+    M, K, N = sp["M"], sp["K"], sp["N"]
+    A, B = inputs.make_inputs(sp)
+    C0 = inputs.make_c0(sp) if sp["acc"] else None
+    got = gu.run_rect(A, B, sp["s"], sp["dtype"], sp["out"], K, N, N, C0=C0)
+    rows = sampled_rows(M, 2)
+    rep = compare.check(sp["dtype"], sp["out"], inputs.bits(A), inputs.bits(B), got[rows],
+                        rows=rows, C0=None if C0 is None else to_np_c0(C0, sp["out"]))
+    print(name, rep)
