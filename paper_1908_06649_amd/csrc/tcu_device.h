@@ -214,4 +214,20 @@ __device__ __forceinline__ void store_out4(unsigned char *p, Acc v, int valid, b
   }
 }
 
+// Add 4 consecutive partial sums into C at p with device-scope atomic adds
+// (binary32 or int32; split-K partial tiles).  Not for bfloat16 outputs,
+// which must be rounded once from the whole sum.
+template <int DT, typename Acc>
+__device__ __forceinline__ void atomic_add_out4(unsigned char *p, Acc v) {
+  static_assert(DT != TCU_BF16_BF16, "bfloat16 outputs are never split");
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    if constexpr (DT == TCU_I8_I32)
+      __hip_atomic_fetch_add((int *)p + e, (int)v[e], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    else
+      __hip_atomic_fetch_add((float *)p + e, (float)v[e], __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
 }  // namespace tcu

@@ -345,7 +345,7 @@ template <int DT, int kRing>
 __global__ __attribute__((amdgpu_flat_work_group_size(512, 512), amdgpu_waves_per_eu(2, 2))) void
 gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restrict__ B,
                unsigned char *__restrict__ C, int K, int64_t lda, int64_t ldb, int64_t ldc,
-               int accum, int tiles_m, int tiles_n) {
+               int accum, int tiles_m, int tiles_n, int nsplit) {
   constexpr bool kI8 = (DT == TCU_I8_I32);
   constexpr int ES = in_bytes(DT);
   constexpr int OB = out_bytes(DT);
@@ -359,29 +359,37 @@ gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restr
   __shared__ __attribute__((aligned(1024))) unsigned char sA[kRing * kFastStage];
   __shared__ __attribute__((aligned(1024))) unsigned char sB[kRing * kFastStage];
 
-  const int total = tiles_m * tiles_n;
-  int tile = blockIdx.x;
-  int m0, n0;
-  auto place = [&](int t) {
-    int tm, tn;
-    map_tile(t, tiles_m, tiles_n, tm, tn);
-    m0 = tm * 256;
-    n0 = tn * 256;
-  };
-  place(tile);
+  // Work items: (K slice, output tile) pairs, slice-major so that the
+  // workgroups running at one time share the K range of their A and B
+  // panels.  With nsplit > 1 each item sums one contiguous range of whole
+  // stages (about nk_all / nsplit strips A_i of the unit) and adds its
+  // partial tile into C atomically.
+  const int tiles = tiles_m * tiles_n;
+  const int total = tiles * nsplit;
+  const int nk_all = K / KE;
   const int64_t lda_b = lda * ES, ldb_b = ldb * ES, ldc_b = ldc * OB;
   const int lane = threadIdx.x & 63;
   const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int grp = wid >> 2, q = wid & 3;
   const int r = lane & 15, g = lane >> 4;
-  const int nk = K / KE;
-
+  int item = blockIdx.x;
+  int m0, n0, nk;
   // This wave's DMA share of a stage: group 0 -> A blocks 4q..4q+3 (16 rows
   // each, stored chunk-major), group 1 -> B blocks 4q..4q+3 (1 KiB each).
   // Wave-uniform 64-bit base + per-lane 32-bit offsets (saddr form).
   const unsigned char *gbase;
-  auto set_gbase = [&]() { gbase = grp == 0 ? A + (int64_t)m0 * lda_b : B + (int64_t)n0 * ES; };
-  set_gbase();
+  auto place = [&](int w) {
+    const int slice = w / tiles;
+    int tm, tn;
+    map_tile(w - slice * tiles, tiles_m, tiles_n, tm, tn);
+    m0 = tm * 256;
+    n0 = tn * 256;
+    const int s_begin = (int)((int64_t)nk_all * slice / nsplit);
+    nk = (int)((int64_t)nk_all * (slice + 1) / nsplit) - s_begin;
+    gbase = grp == 0 ? A + (int64_t)m0 * lda_b + (int64_t)s_begin * kFastKB
+                     : B + (int64_t)n0 * ES + (int64_t)s_begin * KE * ldb_b;
+  };
+  place(item);
   const int64_t gstep = grp == 0 ? (int64_t)kFastKB : (int64_t)KE * ldb_b;
   unsigned voff[kDma];
 #pragma unroll
@@ -519,17 +527,36 @@ gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restr
       for (int fm = 0; fm < FM; ++fm) {
         const int row = m0 + grp * 128 + fm * 16 + r;
         const int col = n0 + q * 64 + fn * 16 + 4 * g;
-        store_out4<DT, true>(C + (int64_t)row * ldc_b + (int64_t)col * OB, acc[fn][fm], 4,
-                             accum != 0);
+        unsigned char *p = C + (int64_t)row * ldc_b + (int64_t)col * OB;
+        if constexpr (DT != TCU_BF16_BF16) {
+          if (nsplit > 1) {
+            atomic_add_out4<DT>(p, acc[fn][fm]);
+            continue;
+          }
+        }
+        store_out4<DT, true>(p, acc[fn][fm], 4, accum != 0);
       }
     }
     // Every wave finished reading the ring at the last barrier of the loop.
-    tile += gridDim.x;
-    if (tile >= total) break;
-    place(tile);
-    set_gbase();
+    item += gridDim.x;
+    if (item >= total) break;
+    place(item);
     for (int s0 = 0; s0 < kRing; ++s0)
       if (s0 < nk) issue(s0, s0);
+  }
+}
+
+// Zero the rows x row_bytes view at C (row pitch ldc_b bytes; row_bytes and
+// ldc_b multiples of 16): the starting value of a split-K product that
+// overwrites C.
+__global__ __launch_bounds__(256) void zero_fill_kernel(unsigned char *__restrict__ C, int64_t rows,
+                                                        int64_t row_bytes, int64_t ldc_b) {
+  const int64_t per_row = row_bytes / 16;
+  const int64_t total = rows * per_row;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t rr = i / per_row;
+    *(u32x4 *)(C + rr * ldc_b + (i - rr * per_row) * 16) = u32x4{0u, 0u, 0u, 0u};
   }
 }
 
@@ -564,22 +591,48 @@ hipError_t launch_dt(const RectArgs &a, hipStream_t stream, int num_cus) {
   const GemmPath path = gemm_path();
   // The full-tile kernel: whole 256 x 256 tiles, whole K stages, and the
   // per-lane 32-bit DMA offsets within a stage in range.
-  const bool fast_ok = vec && a.M % 256 == 0 && a.N % 256 == 0 && a.K % KE == 0 && a.K > 0 &&
-                       256 * a.lda * ES < ((int64_t)1 << 32) &&
+  const bool fast_ok = path != GemmPath::kGeneral && vec && a.M % 256 == 0 && a.N % 256 == 0 &&
+                       a.K % KE == 0 && a.K > 0 && 256 * a.lda * ES < ((int64_t)1 << 32) &&
                        KE * a.ldb * ES < ((int64_t)1 << 32);
-  if (fast_ok && (path == GemmPath::kFast || (path == GemmPath::kAuto && big_tiles >= num_cus))) {
+  // Split-K: when the full-tile kernel has fewer tiles than CUs and a long
+  // K, the stages are cut into nsplit ranges processed by separate work
+  // items whose partial tiles are added into C atomically (binary32 or
+  // int32 outputs only: a bfloat16 output is rounded once from the whole
+  // sum).  Each range keeps at least kMinSplitStages stages.
+  constexpr int kMinSplitStages = 32;
+  int nsplit = 1;
+  if (fast_ok && DT != TCU_BF16_BF16 && big_tiles < num_cus) {
+    const int64_t want = (num_cus + big_tiles - 1) / big_tiles;
+    const int64_t cap = (a.K / KE) / kMinSplitStages;
+    nsplit = (int)(want < cap ? want : cap);
+    if (nsplit < 1) nsplit = 1;
+  }
+  const char *sv = std::getenv("TCU_SPLIT_K");   // tests: force a split count
+  if (sv && fast_ok && DT != TCU_BF16_BF16 && std::atoi(sv) > 0) {
+    nsplit = std::atoi(sv);
+    if (nsplit > a.K / KE) nsplit = (int)(a.K / KE);
+  }
+  if (fast_ok && (path == GemmPath::kFast || nsplit > 1 ||
+                  (path == GemmPath::kAuto && big_tiles >= num_cus))) {
     const int tm = (int)(a.M / 256), tn = (int)(a.N / 256);
+    if (nsplit > 1 && !a.accum) {
+      hipLaunchKernelGGL(zero_fill_kernel, dim3(num_cus * 4), dim3(256), 0, stream,
+                         (unsigned char *)a.C, a.M, a.N * OB, a.ldc * OB);
+      const hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+    }
     // Persistent grid: one workgroup per CU (the LDS ring admits one), each
     // walking tiles blockIdx, blockIdx + grid, ...  TCU_PP_GRID=<g> sets the
     // grid size instead (tests use a tiny grid to give every workgroup many
     // tiles).
     const char *gv = std::getenv("TCU_PP_GRID");
     const int want = gv && std::atoi(gv) > 0 ? std::atoi(gv) : num_cus;
-    const int grid = want < tm * tn ? want : tm * tn;
+    const int items = tm * tn * nsplit;
+    const int grid = want < items ? want : items;
     hipLaunchKernelGGL((gemm_pp_kernel<DT, TCU_RING>), dim3(grid), dim3(512), 0, stream,
                        (const unsigned char *)a.A, (const unsigned char *)a.B,
                        (unsigned char *)a.C, (int)a.K, a.lda, a.ldb, a.ldc, a.accum ? 1 : 0,
-                       tm, tn);
+                       tm, tn, nsplit);
     return hipGetLastError();
   }
   // Element-wise operand access (pitches not multiples of 16 bytes).

@@ -91,6 +91,20 @@ def test_rect_full_tiles_many_per_workgroup(din, out, accumulate, monkeypatch):
     run_and_check(768, 512, 1024, din, out, 32, "padded", accumulate, seed=12)
 
 
+@pytest.mark.parametrize("nsplit", [2, 3, 7])
+@pytest.mark.parametrize("din,out", PAIRS)
+@pytest.mark.parametrize("accumulate", [False, True])
+def test_rect_split_k(din, out, accumulate, nsplit, monkeypatch):
+    """Split-K on the full-tile kernel: the stages cut into nsplit ranges
+    whose partial tiles are added into C atomically (after zeroing C when
+    overwriting).  int32 stays bit-exact; a bfloat16 output is never split
+    (rounded once), so it must pass the single-rounding check."""
+    monkeypatch.setenv("TCU_GEMM_KERNEL", "fast")
+    monkeypatch.setenv("TCU_SPLIT_K", str(nsplit))
+    run_and_check(512, 1344 if din != "i8" else 2688, 256, din, out, 32, "padded", accumulate,
+                  seed=40 + nsplit)
+
+
 @pytest.mark.parametrize("s", [16, 32])
 @pytest.mark.parametrize("din,out", PAIRS)
 @pytest.mark.parametrize("M", [7, 16, 4099])
