@@ -13,6 +13,9 @@ numpy in/out:
   A so that large cases can be checked on sampled rows.
 * ``f16_to_f64``, ``bf16_to_f64`` -- format decoders.
 * ``f64_to_bf16`` -- one-step round-to-nearest-even to bfloat16 bit patterns.
+* ``poly_eval(coef, points, dtype)`` -- A(x) = sum_h a_h x^h at every point
+  (Theorem 11, Section 4.8), in binary64 on the decoded 16-bit inputs, with
+  the magnitude sum sum_h |a_h| |x|^h.
 * ``mm_acc(A, B, C0, dtype, out)`` -- the accumulating form ``C0 + A*B``
   that the D functions of Sections 4.2 and 4.3 ask of the unit
   (X <- X + Y*Z); C0 holds stored output values ('f32', 'bf16' bits or
@@ -57,6 +60,8 @@ def _load():
     lib.oracle_mm_f64.restype = ctypes.c_int
     lib.oracle_mm_i64.argtypes = [vp, vp, i64, i64, i64, vp, i64, vp]
     lib.oracle_mm_i64.restype = ctypes.c_int
+    lib.oracle_poly_eval.argtypes = [ctypes.c_int, vp, i64, vp, i64, vp, vp]
+    lib.oracle_poly_eval.restype = ctypes.c_int
     lib.oracle_threads.argtypes = []
     lib.oracle_threads.restype = ctypes.c_int
     _lib = lib
@@ -148,3 +153,19 @@ def mm_acc(A: np.ndarray, B: np.ndarray, C0: np.ndarray, dtype: str, out: str,
     if rows is not None:
         c0 = c0[np.asarray(rows, dtype=np.int64)]
     return c0 + prod
+
+
+def poly_eval(coef: np.ndarray, points: np.ndarray, dtype: str):
+    """(values, magnitudes): A(x_i) = sum_h a_h x_i^h and sum_h |a_h| |x_i|^h
+    for every point, from the stored 16-bit coefficients and points."""
+    if dtype not in ("f16", "bf16"):
+        raise ValueError("polynomial evaluation takes f16 or bf16 inputs")
+    a = np.ascontiguousarray(coef).view(np.uint16).ravel()
+    x = np.ascontiguousarray(points).view(np.uint16).ravel()
+    val = np.empty(x.size, dtype=np.float64)
+    mag = np.empty(x.size, dtype=np.float64)
+    rc = _load().oracle_poly_eval(_DTYPES[dtype], _ptr(a), a.size, _ptr(x), x.size,
+                                  _ptr(val), _ptr(mag))
+    if rc != 0:
+        raise ValueError("oracle rejected its arguments")
+    return val, mag

@@ -235,3 +235,38 @@ int oracle_threads(void)
     return 1;
 #endif
 }
+
+/* ------------------------------------------ batch polynomial evaluation */
+/*
+ * Theorem 11 (Section 4.8) evaluates A(x) = sum_{h<n} a_h x^h at p points.
+ * Its method (power matrix X times the coefficient matrix in unit-sized
+ * blocks, then a combine over the blocks' columns) only regroups that sum,
+ * so the oracle is the definition itself: for every point, the terms
+ * a_h * x^h for h = 0, 1, ..., n-1 in that order, the power kept by the
+ * recurrence x^0 = 1, x^(h+1) = x^h * x, everything in binary64 on the
+ * decoded 16-bit inputs.  It also returns the magnitude sum
+ * sum_h |a_h| |x|^h that bounds the rounding error of any evaluation.
+ */
+int oracle_poly_eval(int dtype, const void *coef, int64_t n, const void *pts, int64_t p,
+                     double *value, double *magnitude)
+{
+    if (dtype != ORC_F16 && dtype != ORC_BF16) return -1;
+    if (n < 0 || p < 0) return -1;
+    double *a = (double *)malloc(sizeof(double) * (size_t)(n > 0 ? n : 1));
+    if (!a) return -2;
+    for (int64_t h = 0; h < n; ++h) a[h] = decode_one(dtype, coef, h);
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < p; ++i) {
+        const double x = decode_one(dtype, pts, i);
+        double power = 1.0, sum = 0.0, mag = 0.0;
+        for (int64_t h = 0; h < n; ++h) {
+            sum += a[h] * power;
+            mag += fabs(a[h]) * fabs(power);
+            power *= x;
+        }
+        value[i] = sum;
+        magnitude[i] = mag;
+    }
+    free(a);
+    return 0;
+}
