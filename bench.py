@@ -16,6 +16,9 @@ JSON line:
   secondary  the other workloads measured the same way: the very tall
              bf16 native call (GB/s vs HBM peak), the int8 product (TOP/s),
              the 4096 x 16 native call and the N = 1024 fp16 product
+  poly       batch polynomial evaluation (tcu_poly_eval, Theorem 11) on 2^24
+             points with 4096 coefficients: TFLOP/s of the method's 2pn
+             multiply-adds vs the bf16 matrix-core peak
   rect       the rectangular / accumulating product (tcu_gemm_rect):
              Corollary 1's sqrt(n) x r by r x sqrt(n) with r below and above
              sqrt(n), accumulating into C, and an order-8200 product that
@@ -56,7 +59,8 @@ PROFILES = os.path.join(ROOT, "profiles")
 
 
 def kernel_sources(kind: str):
-    main = "tcu_gemm.hip" if kind in ("gemm", "rect") else "tcu_tall.hip"
+    main = {"gemm": "tcu_gemm.hip", "rect": "tcu_gemm.hip", "poly": "tcu_poly.hip"}.get(
+        kind, "tcu_tall.hip")
     return [os.path.join(CSRC, f) for f in (main, "tcu_device.h")]
 
 
@@ -97,6 +101,9 @@ def algorithmic(spec: dict):
         n, s = spec["n"], spec["s"]
         return 2.0 * n * s * s, n * s * ib + s * s * ib + n * s * ob
     del inputs
+    if spec["kind"] == "poly":
+        n, p = spec["n"], spec["p"]
+        return 2.0 * n * p, n * ib + p * ib + p * ob
     if spec["kind"] == "rect":
         M, K, N = spec["M"], spec["K"], spec["N"]
         c_io = 2 if spec.get("acc") else 1          # C read too when accumulating
@@ -112,8 +119,16 @@ class Workload:
         import torch
         from paper_1908_06649_amd import inputs, tcu
         self.name = name
-        self.spec = inputs.WORKLOADS.get(name) or inputs.RECT_WORKLOADS[name]
+        self.spec = (inputs.WORKLOADS.get(name) or inputs.RECT_WORKLOADS.get(name)
+                     or inputs.POLY_WORKLOADS[name])
         self.tcu = tcu
+        self.s = self.spec["s"]
+        if self.spec["kind"] == "poly":
+            self.A, self.B = inputs.make_poly_inputs(self.spec)     # coefficients, points
+            self.dA, self.dB = self.A.cuda(), self.B.cuda()
+            self.C = torch.empty(self.spec["p"], dtype=inputs.TORCH_DTYPE[self.spec["out"]],
+                                 device="cuda")
+            return
         self.A, self.B = inputs.make_inputs(self.spec)
         self.dA, self.dB = self.A.cuda(), self.B.cuda()
         _, _, c_shape = inputs.shapes(self.spec)
@@ -128,6 +143,8 @@ class Workload:
         sp = self.spec
         if sp["kind"] == "gemm":
             self.tcu.tcu_gemm(self.dA, self.dB, self.C, sp["N"])
+        elif sp["kind"] == "poly":
+            self.tcu.tcu_poly_eval(self.dA, sp["n"], self.dB, sp["p"], self.C)
         elif sp["kind"] == "rect":
             M, K, N = sp["M"], sp["K"], sp["N"]
             self.tcu.tcu_gemm_rect(self.dA, K, self.dB, N, self.C, N, M, K, N,
@@ -186,7 +203,7 @@ def measure(name: str, steps: int, warmup: int) -> dict:
     kind = sp["kind"]
     out = {"workload": name, "ms_per_call": ms, "calls": calls, "square_calls": squares,
            "model_work": work}
-    if kind in ("gemm", "rect"):
+    if kind in ("gemm", "rect", "poly"):
         tput = flops / (ms * 1e-3) / 1e12
         peak = PEAK[sp["dtype"]]
         out.update({"value": tput, "unit": "TOP/s" if sp["dtype"] == "i8" else "TFLOP/s",
@@ -197,6 +214,9 @@ def measure(name: str, steps: int, warmup: int) -> dict:
                     "algorithmic_flops": flops, "compulsory_bytes": nbytes})
         if kind == "gemm":
             out["calls_theorem2"] = (sp["N"] // sp["s"]) ** 2
+        elif kind == "poly":   # Theorem 11's n/m calls, each issued for X_hi and X_lo
+            out["calls_theorem11"] = 2 * -(-sp["n"] // (sp["s"] * sp["s"]))
+            out["points_per_s"] = sp["p"] / (ms * 1e-3)
         else:   # Corollary 1 on the zero-padded operands
             out["calls_corollary1"] = -(-sp["K"] // sp["s"]) * -(-sp["N"] // sp["s"])
     else:
@@ -294,6 +314,7 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default=HEADLINE)
     ap.add_argument("--no-rect", action="store_true")
+    ap.add_argument("--no-poly", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--copy-probe", action="store_true")
@@ -313,8 +334,9 @@ def main() -> int:
     if args.copy_probe:
         copy_probe()
         return 0
-    if args.workload not in inputs.WORKLOADS and args.workload not in inputs.RECT_WORKLOADS:
-        names = sorted(inputs.WORKLOADS) + sorted(inputs.RECT_WORKLOADS)
+    known = {**inputs.WORKLOADS, **inputs.RECT_WORKLOADS, **inputs.POLY_WORKLOADS}
+    if args.workload not in known:
+        names = sorted(known)
         print(f"unknown workload {args.workload}; choose from {names}", file=sys.stderr)
         return 2
 
@@ -335,9 +357,10 @@ def main() -> int:
         "dtype": sp["dtype"],
         "data": "synthetic (seeded i.i.d. matrices; the paper has no datasets)",
         "config": {"workload": args.workload,
-                   **{k: sp[k] for k in ("kind", "M", "K", "N", "n", "s", "acc") if k in sp},
+                   **{k: sp[k] for k in ("kind", "M", "K", "N", "n", "p", "s", "acc") if k in sp},
                    "dtype_in": sp["dtype"], "dtype_out": sp["out"],
-                   "distribution": sp["dist"], "seed": sp["seed"]},
+                   "distribution": sp.get("dist", "coefficients N(0,1), points U[-1,1)"),
+                   "seed": sp["seed"]},
         "roofline": main_res["roofline"],
     }
     cost = {k: main_res[k] for k in ("calls", "square_calls", "model_work") if k in main_res}
@@ -377,8 +400,21 @@ def main() -> int:
                                             "calls_corollary1", "square_calls", "model_work")}
             torch.cuda.empty_cache()
         result["rect"] = rect
+    if not args.no_poly:
+        poly = {}
+        for name in inputs.POLY_WORKLOADS:
+            if name == args.workload:
+                continue
+            r = measure(name, args.steps, max(args.warmup, 5))
+            r.pop("_workload")
+            poly[name] = {k: r[k] for k in ("value", "unit", "ms_per_call", "roofline", "calls",
+                                            "calls_theorem11", "points_per_s", "square_calls",
+                                            "model_work")}
+            torch.cuda.empty_cache()
+        result["poly"] = poly
     result["cost_model"] = cost
-    result["kernel_source_sha256"] = {"gemm": kernel_hash("gemm"), "tall": kernel_hash("tall")}
+    result["kernel_source_sha256"] = {"gemm": kernel_hash("gemm"), "tall": kernel_hash("tall"),
+                                      "poly": kernel_hash("poly")}
     print(json.dumps(result), flush=True)
     return 0
 

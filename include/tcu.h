@@ -13,6 +13,9 @@
  *   - tcu_gemm: the dense N x N multiplication of Theorem 2 (Section 4.1),
  *     built from (N/s)^2 such calls: A is cut into N x s vertical strips A_i,
  *     B into s x s blocks B_{i,j}, and output strip j is sum_i A_i * B_{i,j}.
+ *   - tcu_gemm_rect: the same decomposition for rectangular, strided and
+ *     accumulating products (Corollary 1; the D functions' update).
+ *   - tcu_poly_eval: batch polynomial evaluation (Theorem 11).
  *
  * Throughout, s = sqrt(m) is the unit size (a machine parameter of the
  * model), n is the row count of a tall call and N the order of the square
@@ -186,6 +189,39 @@ int tcu_gemm_rect(const void *A, int64_t lda, const void *B, int64_t ldb, void *
 int tcu_gemm_rect_ex(const void *A, int64_t lda, const void *B, int64_t ldb, void *C,
                      int64_t ldc, int64_t M, int64_t K, int64_t N, int flags, int s, int dtype,
                      void *hip_stream);
+
+/* ---- batch polynomial evaluation (Theorem 11, Section 4.8) ----
+ *
+ * out[i] = A(points[i]) = sum_{h<n} coef[h] * points[i]^h, for 0 <= i < p.
+ *
+ * Theorem 11's method: the p x s matrix X of the powers x_i^0 .. x_i^(s-1),
+ * times the s x (n/s) matrix whose column j holds a_(js) .. a_(js+s-1)
+ * (the coefficients read column-major), cut into s x s blocks -- ceil(n/m)
+ * tall calls of p rows -- followed by A(x_i) = sum_j C[i][j] x_i^(js).
+ * The powers are formed in binary32 and handed to the unit as the sum of
+ * two words of the input type (X = X_hi + X_lo), so every call is issued
+ * twice; the combine runs in binary32 and C is never stored.  n and p need
+ * not be multiples of s (zero padding; the theorem assumes them).
+ *   coef: n input elements (binary16 or bfloat16, the unit's input type).
+ *   n: number of coefficients (degree n-1); 0 <= n <= TCU_MAX_ROWS; n = 0
+ *      gives zeros.
+ *   points: p input elements (same type); 0 <= p <= TCU_MAX_ROWS; p = 0 is
+ *      a no-op.
+ *   out: p output elements: binary32 (TCU_F16_F32, TCU_BF16_F32) or
+ *      bfloat16 rounded once to nearest even (TCU_BF16_BF16).
+ * The unit size and dtype come from tcu_get_unit() / tcu_get_dtype()
+ * (TCU_I8_I32 is TCU_ERR_UNSUPPORTED).  Results are meaningful while
+ * |x|^(n-1) and the partial sums stay in binary32 range (the theorem
+ * assumes no overflow) and, for binary16 inputs, |x|^k < 65504 for
+ * k < min(n, s).
+ * A pointer may be NULL only if its array is empty.  Errors: TCU_ERR_NULL,
+ * TCU_ERR_SHAPE, TCU_ERR_UNSUPPORTED, TCU_ERR_ALIGN (16-byte base
+ * alignment), TCU_ERR_OVERLAP (out overlapping coef or points),
+ * TCU_ERR_NO_DEVICE, TCU_ERR_HIP.
+ * Cost accounting: 2*ceil(n/m) calls of ceil(p/s) square calls each. */
+int tcu_poly_eval(const void *coef, int64_t n, const void *points, int64_t p, void *out);
+int tcu_poly_eval_ex(const void *coef, int64_t n, const void *points, int64_t p, void *out, int s,
+                     int dtype, void *hip_stream);
 
 /* ---- cost accounting (Theorem 2 proof; Section 5 weak model) ----
  * tcu_calls:        logical tensor-unit calls issued (1 per tall call,

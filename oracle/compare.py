@@ -21,7 +21,7 @@ from __future__ import annotations
 
 import numpy as np
 
-from . import decode_out, f64_to_bf16, bf16_to_f64, mm, mm_acc
+from . import decode_out, f64_to_bf16, bf16_to_f64, mm, mm_acc, poly_eval
 
 REL_FROB = 1e-3
 ELEM = 1e-2
@@ -127,3 +127,58 @@ def check(dtype_in: str, dtype_out: str, A_bits, B_bits, got, rows=None, C0=None
     if dtype_out == "bf16":
         return check_bf16(got, ref, absab, K=K)
     return check_float(got, ref, absab)
+
+
+def poly_bound(dtype_in: str, n: int, s: int) -> float:
+    """Relative-to-magnitude error bound of the batch polynomial evaluation
+    (Theorem 11) as the unit computes it, times a safety factor of 4:
+      * X = X_hi + X_lo leaves a residual of at most 2^-18 |x^k| (bfloat16:
+        two nearest roundings of 9 significant bits) or 2^-22 (binary16);
+      * every power is a chain of at most 2 log2(s) + s binary32 products,
+        the block weights y^(s J) a chain of n/s^2 more;
+      * the unit's sums run over s products, the combine over s + n/s^2
+        terms plus two cross-lane additions;
+    each binary32 operation adding at most 2^-24 of the magnitude sum
+    sum_h |a_h| |x|^h."""
+    split = 2.0 ** -18 if dtype_in == "bf16" else 2.0 ** -22
+    ops = 2 * 6 + s + s + 2 * (n // (s * s) + 1) + 8
+    return 4.0 * (split + ops * 2.0 ** -24)
+
+
+def check_poly(dtype_in: str, dtype_out: str, coef_bits, pt_bits, got, s: int,
+               idx=None) -> dict:
+    """Compare GPU polynomial values (numpy float32, or bf16 bits for a
+    bfloat16 output) with the oracle: elementwise
+    |g - A(x)| <= poly_bound * sum_h |a_h||x|^h (+ half a bfloat16 ulp of
+    g for a bfloat16 output), and relative Frobenius error <= 1e-3 against
+    the exact values (1e-3 + 2^-9 for a bfloat16 output: the format's own
+    rounding; a bfloat16 value is also checked elementwise, above, to be a
+    nearest rounding of a value within the bound).
+    idx: the point indices `got` holds (all points when None)."""
+    pts = np.ascontiguousarray(pt_bits).view(np.uint16)
+    if idx is not None:
+        pts = pts[np.asarray(idx, dtype=np.int64)]
+    val, mag = poly_eval(coef_bits, pts, dtype_in)
+    n = np.asarray(coef_bits).size
+    if dtype_out == "bf16":
+        g = bf16_to_f64(np.asarray(got).view(np.uint16))
+        extra = 0.5 * bf16_spacing(g)
+    else:
+        g = np.asarray(got, dtype=np.float64)
+        extra = 0.0
+    err = np.abs(g - val)
+    allow = poly_bound(dtype_in, n, s) * mag + extra
+    denom = np.linalg.norm(val)
+    rel = float(np.linalg.norm(g - val) / denom) if denom > 0 else float(np.linalg.norm(g - val))
+    # one nearest rounding to bfloat16 moves every value by at most 2^-9 of
+    # itself, so the output format adds at most 2^-9 to the relative
+    # Frobenius error against the exact values
+    rel_bar = REL_FROB + (2.0 ** -9 if dtype_out == "bf16" else 0.0)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        ratio = np.where(mag > 0, err / mag, np.where(err > 0, np.inf, 0.0))
+    rep = {"rel_frob": rel, "max_err_over_magnitude": float(ratio.max(initial=0.0)),
+           "bound": poly_bound(dtype_in, n, s), "violations": int((err > allow).sum())}
+    assert np.all(np.isfinite(g)), rep
+    assert rep["violations"] == 0, rep
+    assert rel <= rel_bar, rep
+    return rep

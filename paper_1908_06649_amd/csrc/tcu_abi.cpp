@@ -167,6 +167,18 @@ int validate_rect(const void *A, int64_t lda, const void *B, int64_t ldb, const 
   return TCU_OK;
 }
 
+int validate_poly(const void *coef, int64_t n, const void *pts, int64_t p, const void *out, int s,
+                  int dt) {
+  if (!unit_ok(s) || !dtype_ok(dt) || dt == TCU_I8_I32) return TCU_ERR_UNSUPPORTED;
+  if (n < 0 || p < 0 || n > TCU_MAX_ROWS || p > TCU_MAX_ROWS) return TCU_ERR_SHAPE;
+  // A pointer may be NULL only if its array is empty.
+  if ((!coef && n > 0) || (!pts && p > 0) || (!out && p > 0)) return TCU_ERR_NULL;
+  if (misaligned(coef) || misaligned(pts) || misaligned(out)) return TCU_ERR_ALIGN;
+  const int64_t ob = p * out_size(dt);
+  if (overlap(out, ob, coef, n * 2) || overlap(out, ob, pts, p * 2)) return TCU_ERR_OVERLAP;
+  return TCU_OK;
+}
+
 }  // namespace
 
 TCU_EXPORT int tcu_set_unit(int s) {
@@ -263,6 +275,32 @@ TCU_EXPORT int tcu_gemm_rect(const void *A, int64_t lda, const void *B, int64_t 
                              int64_t ldc, int64_t M, int64_t K, int64_t N, int flags) {
   return tcu_gemm_rect_ex(A, lda, B, ldb, C, ldc, M, K, N, flags, g_cfg.s, g_cfg.dtype,
                           g_cfg.stream);
+}
+
+TCU_EXPORT int tcu_poly_eval_ex(const void *coef, int64_t n, const void *points, int64_t p,
+                                void *out, int s, int dtype, void *hip_stream) {
+  int rc = validate_poly(coef, n, points, p, out, s, dtype);
+  if (rc != TCU_OK) return rc;
+  if (p == 0) return TCU_OK;
+  int num_cus = 0;
+  rc = device_ready(&num_cus);
+  if (rc != TCU_OK) return rc;
+  if (tcu::launch_poly(dtype, s, coef, n, points, p, out, (hipStream_t)hip_stream, num_cus) !=
+      hipSuccess)
+    return TCU_ERR_HIP;
+  // Theorem 11: ceil(n/m) calls of X (p x s) times an s x s coefficient
+  // block, each issued twice (X as the sum of two words of the input type).
+  const int64_t calls = 2 * ((n + (int64_t)s * s - 1) / ((int64_t)s * s));
+  const int64_t row_blocks = (p + s - 1) / s;
+  g_calls.fetch_add(calls, std::memory_order_relaxed);
+  g_square_calls.fetch_add(calls * row_blocks, std::memory_order_relaxed);
+  g_work.fetch_add(calls * row_blocks * s * s, std::memory_order_relaxed);
+  return TCU_OK;
+}
+
+TCU_EXPORT int tcu_poly_eval(const void *coef, int64_t n, const void *points, int64_t p,
+                             void *out) {
+  return tcu_poly_eval_ex(coef, n, points, p, out, g_cfg.s, g_cfg.dtype, g_cfg.stream);
 }
 
 TCU_EXPORT int64_t tcu_calls(void) { return g_calls.load(std::memory_order_relaxed); }

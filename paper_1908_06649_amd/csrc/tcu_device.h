@@ -124,10 +124,12 @@ __device__ __forceinline__ u32x2 lds_read_tr8(const void *p) {
   return bitcast<u32x2>(__builtin_amdgcn_ds_read_tr8_b64_v2i32(TCU_LDS(i32x2, p)));
 }
 
-// binary32 -> bfloat16, round to nearest even (gfx950 v_cvt_pk_bf16_f32).
+// Two binary32 values -> two bfloat16 in one word (lo in bits 0-15), round
+// to nearest even: one gfx950 v_cvt_pk_bf16_f32.
 __device__ __forceinline__ unsigned pack_bf16x2(float lo, float hi) {
-  __bf16 a = (__bf16)lo, b = (__bf16)hi;
-  return (unsigned)bitcast<unsigned short>(a) | ((unsigned)bitcast<unsigned short>(b) << 16);
+  typedef float f32x2 __attribute__((ext_vector_type(2)));
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  return bitcast<unsigned>(__builtin_convertvector(f32x2{lo, hi}, bf16x2));
 }
 
 // bfloat16 bit pattern -> binary32 (exact).

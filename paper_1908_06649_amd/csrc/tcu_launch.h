@@ -27,4 +27,9 @@ struct RectArgs {
 };
 hipError_t launch_rect(int dtype, int s, const RectArgs &args, hipStream_t stream, int num_cus);
 
+// Batch polynomial evaluation: out[i] = sum_{h<n} coef[h] * pts[i]^h for
+// i < np, 16-bit inputs (dtype TCU_F16_F32, TCU_BF16_F32 or TCU_BF16_BF16).
+hipError_t launch_poly(int dtype, int s, const void *coef, int64_t n, const void *pts, int64_t np,
+                       void *out, hipStream_t stream, int num_cus);
+
 }  // namespace tcu

@@ -1,0 +1,254 @@
+// Batch polynomial evaluation of Theorem 11 (Section 4.8):
+// out[i] = A(x_i) = sum_{h<n} a_h x_i^h for p points x_i.
+//
+// The theorem's method, fused into one launch:
+//   * X (p x s): row i holds x_i^0 .. x_i^(s-1);
+//   * the coefficients, read column-major, form the s x (n/s) matrix with
+//     entry (k, j) = a_(k + j s); its s x s blocks are the unit's weights;
+//   * C = X times that matrix, as n/m tall calls of p rows (one per block);
+//   * A(x_i) = sum_j C[i][j] x_i^(j s).
+// Each wave owns chunks of 16 points, one point per matrix-core column:
+//   * it computes the powers of its points in binary32 (the theorem's
+//     initial exponentiation, as a ladder of squarings shared by all lanes
+//     plus a short chain per lane) and hands X to the unit as an unevaluated
+//     sum of two words of the input type, X = X_hi + X_lo, so the unit
+//     multiplies X to about 2^-16 (bfloat16) or 2^-22 (binary16) relative
+//     accuracy instead of one rounding of the input type -- the model
+//     multiplies exactly, and one 16-bit rounding of x^k would dominate
+//     the error;
+//   * for every block it loads the block's weights once (16-byte contiguous
+//     runs of coefficients, shared by the wave's U chunks) and issues two
+//     matrix-core products per 16-column half (X_hi, then X_lo into the
+//     same binary32 accumulators);
+//   * lane (r, g) then holds C[point r][columns 16h + 4g + i] of the block
+//     and forms t = sum of them with weights y^(16h + 4g + i), y = x^s; the
+//     blocks are walked last to first and combined by Horner's rule in
+//     y^s (acc = acc * y^s + t) -- the final combine, never writing C;
+//   * the four lanes holding one point add their sums (cross-lane
+//     exchange) and one stores A(x_i).
+// Coefficients past n and points past p are zero padding.  Results are
+// meaningful while |x|^(n-1) and the partial sums stay within binary32
+// range (the theorem assumes evaluation without overflow); for binary16
+// inputs also x^k, k < min(n, s), must be representable in binary16.
+#include "tcu_device.h"
+#include "tcu_launch.h"
+
+namespace tcu {
+namespace {
+
+constexpr int kPolyThreads = 256;  // 4 waves per workgroup
+#ifndef TCU_POLY_U
+#define TCU_POLY_U 4               // 16-point chunks per wave and pass
+#endif
+
+template <int DT>
+__device__ __forceinline__ float in_to_f32(unsigned bits16) {
+  if constexpr (DT == TCU_F16_F32)
+    return (float)__builtin_bit_cast(_Float16, (unsigned short)bits16);
+  else
+    return bf16_to_f32(bits16);
+}
+
+// Two binary32 values as the high ("hi") and remainder ("lo") words of the
+// input type, packed two per 32-bit word: hi = v rounded to the input type,
+// lo = (v - hi) rounded again (v - hi is exact in binary32).  bfloat16 uses
+// the round-to-nearest-even pack convert; binary16 the packed
+// round-toward-zero convert (any rounding of hi leaves an exact remainder).
+template <int DT>
+__device__ __forceinline__ void split2(float v0, float v1, unsigned &hi, unsigned &lo) {
+  if constexpr (DT == TCU_F16_F32) {
+    hi = bitcast<unsigned>(__builtin_amdgcn_cvt_pkrtz(v0, v1));
+    const float h0 = (float)bitcast<_Float16>((unsigned short)(hi & 0xffffu));
+    const float h1 = (float)bitcast<_Float16>((unsigned short)(hi >> 16));
+    lo = bitcast<unsigned>(__builtin_amdgcn_cvt_pkrtz(v0 - h0, v1 - h1));
+  } else {
+    hi = pack_bf16x2(v0, v1);
+    const float h0 = __builtin_bit_cast(float, hi << 16);
+    const float h1 = __builtin_bit_cast(float, hi & 0xffff0000u);
+    lo = pack_bf16x2(v0 - h0, v1 - h1);
+  }
+}
+
+// b^(step * g) for lane group g = 0..3 from the ladder b^step, b^(2 step):
+// two selects and one product (exact when a factor is 1), no branches.
+__device__ __forceinline__ float pow_group(int g, float b1, float b2) {
+  const float f1 = (g & 1) ? b1 : 1.f;
+  const float f2 = (g & 2) ? b2 : 1.f;
+  return f1 * f2;
+}
+
+template <int DT, int S, int U>
+__global__ __launch_bounds__(kPolyThreads) void poly_kernel(const unsigned char *__restrict__ coef,
+                                                            int64_t n,
+                                                            const unsigned char *__restrict__ pts,
+                                                            int64_t np,
+                                                            unsigned char *__restrict__ out,
+                                                            int64_t nchunks, int64_t nblocks) {
+  // Powers a shorter polynomial never uses (k >= n in X, output columns
+  // j >= ceil(n/S) in the combine) are replaced by zeros rather than
+  // computed, so they cannot overflow where the polynomial itself does not.
+  const int64_t ncols = (n + S - 1) / S;
+  constexpr int kRun = S == 32 ? 8 : 4;  // contracted elements per lane
+  constexpr int kH = S / 16;             // 16-column halves of a block
+  typedef typename std::conditional<kRun == 8, u32x4, u32x2>::type Run;
+  constexpr int kWords = kRun / 2;
+
+  const int lane = threadIdx.x & 63;
+  const int r = lane & 15, g = lane >> 4;
+  const int64_t wave = (int64_t)blockIdx.x * (kPolyThreads / 64) + (threadIdx.x >> 6);
+  const int64_t nwaves = (int64_t)gridDim.x * (kPolyThreads / 64);
+  const unsigned short *pt16 = (const unsigned short *)pts;
+  const unsigned short *cf16 = (const unsigned short *)coef;
+
+  for (int64_t t0 = wave * U; t0 < nchunks; t0 += nwaves * U) {
+    Run xh[U], xl[U];
+    float w[U][kH][4];
+    float acc[U], ystep[U];
+    // All U points first (clamped index, then a select), so the loads are
+    // in flight together.
+    unsigned short praw[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t idx = (t0 + u) * 16 + r;
+      praw[u] = pt16[idx < np ? idx : np - 1];
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t idx = (t0 + u) * 16 + r;
+      const float x = idx < np ? in_to_f32<DT>(praw[u]) : 0.f;
+      // Power ladder (same products in every lane): x^2 .. x^16, y = x^S.
+      const float x2 = x * x, x4 = x2 * x2, x8 = x4 * x4, x16 = x8 * x8;
+      // X fragment: x^(kRun g + e), e < kRun, as hi + lo words.
+      float pw[kRun];
+      pw[0] = kRun == 8 ? pow_group(g, x8, x16) : pow_group(g, x4, x8);
+#pragma unroll
+      for (int e = 1; e < kRun; ++e) pw[e] = pw[e - 1] * x;
+      if (n < S) {   // powers past the polynomial's degree are not used
+#pragma unroll
+        for (int e = 0; e < kRun; ++e) pw[e] = kRun * g + e < n ? pw[e] : 0.f;
+      }
+#pragma unroll
+      for (int q = 0; q < kWords; ++q) {
+        unsigned hi, lo;
+        split2<DT>(pw[2 * q], pw[2 * q + 1], hi, lo);
+        xh[u][q] = hi;
+        xl[u][q] = lo;
+      }
+      // Combine weights y^(16h + 4g + i) and the block step y^S.
+      const float y = S == 32 ? x16 * x16 : x16;
+      const float y2 = y * y, y4 = y2 * y2, y8 = y4 * y4, y16 = y8 * y8;
+      const float wv = pow_group(g, y4, y8);
+#pragma unroll
+      for (int h = 0; h < kH; ++h) {
+        float v = h == 0 ? wv : wv * y16;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          w[u][h][i] = v;
+          v *= y;
+        }
+      }
+      if (ncols < S) {   // output columns past ceil(n/S) are not used
+#pragma unroll
+        for (int h = 0; h < kH; ++h)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) w[u][h][i] = 16 * h + 4 * g + i < ncols ? w[u][h][i] : 0.f;
+      }
+      ystep[u] = S == 32 ? y16 * y16 : y16;
+      acc[u] = 0.f;
+    }
+
+    // Weights of block J: row 16h + r of the unit operand is output column
+    // J*S + 16h + r, i.e. the S coefficients starting at (J*S + 16h + r)*S;
+    // this lane's run starts kRun*g further.  Blocks wholly inside the
+    // coefficient array (a wave-uniform test) take plain vector loads.
+    auto load_block = [&](int64_t J, Run (&wb)[kH]) __attribute__((always_inline)) {
+      const bool full = (J + 1) * S * S <= n;
+#pragma unroll
+      for (int h = 0; h < kH; ++h) {
+        const int64_t base = (J * S + 16 * h + r) * S + kRun * g;
+        if (full) {
+          wb[h] = *(const Run *)(cf16 + base);
+        } else {
+          const int64_t left = n - base;
+          unsigned ww[kWords];
+#pragma unroll
+          for (int q = 0; q < kWords; ++q) ww[q] = 0;
+#pragma unroll
+          for (int e = 0; e < kRun; ++e)
+            if (e < left) ww[e >> 1] |= (unsigned)cf16[base + e] << (16 * (e & 1));
+#pragma unroll
+          for (int q = 0; q < kWords; ++q) wb[h][q] = ww[q];
+        }
+      }
+    };
+    for (int64_t J = nblocks - 1; J >= 0; --J) {
+      Run wf[kH];
+      load_block(J, wf);
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        float t = 0.f;
+#pragma unroll
+        for (int h = 0; h < kH; ++h) {
+          f32x4 d;
+          if constexpr (S == 32) {
+            d = mfma_k32(DT, wf[h], xh[u], f32x4{0.f, 0.f, 0.f, 0.f});
+            d = mfma_k32(DT, wf[h], xl[u], d);
+          } else {
+            d = mfma_k16(DT, wf[h], xh[u], f32x4{0.f, 0.f, 0.f, 0.f});
+            d = mfma_k16(DT, wf[h], xl[u], d);
+          }
+#pragma unroll
+          for (int i = 0; i < 4; ++i) t += d[i] * w[u][h][i];
+        }
+        // Horner over the blocks, last block first: acc = acc * y^S + t.
+        acc[u] = J == nblocks - 1 ? t : acc[u] * ystep[u] + t;
+      }
+    }
+
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      float v = acc[u];
+      v += __shfl_xor(v, 16);
+      v += __shfl_xor(v, 32);
+      const int64_t idx = (t0 + u) * 16 + r;
+      if (g == 0 && idx < np) {
+        if constexpr (DT == TCU_BF16_BF16)
+          ((unsigned short *)out)[idx] = (unsigned short)(pack_bf16x2(v, 0.f) & 0xffffu);
+        else
+          ((float *)out)[idx] = v;
+      }
+    }
+  }
+}
+
+template <int DT, int S>
+hipError_t launch_poly_one(const void *coef, int64_t n, const void *pts, int64_t np, void *out,
+                           hipStream_t stream, int num_cus) {
+  constexpr int U = TCU_POLY_U;
+  const int64_t nchunks = (np + 15) / 16;
+  const int64_t nblocks = (n + (int64_t)S * S - 1) / ((int64_t)S * S);
+  const int64_t want = (nchunks + 4 * U - 1) / (4 * U);
+  const int64_t cap = (int64_t)num_cus * 4;
+  const int blocks = (int)(want < cap ? want : cap);
+  hipLaunchKernelGGL((poly_kernel<DT, S, U>), dim3(blocks), dim3(kPolyThreads), 0, stream,
+                     (const unsigned char *)coef, n, (const unsigned char *)pts, np,
+                     (unsigned char *)out, nchunks, nblocks);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_poly(int dtype, int s, const void *coef, int64_t n, const void *pts, int64_t np,
+                       void *out, hipStream_t stream, int num_cus) {
+  switch (dtype * 2 + (s == 32 ? 1 : 0)) {
+    case TCU_F16_F32 * 2 + 0: return launch_poly_one<TCU_F16_F32, 16>(coef, n, pts, np, out, stream, num_cus);
+    case TCU_F16_F32 * 2 + 1: return launch_poly_one<TCU_F16_F32, 32>(coef, n, pts, np, out, stream, num_cus);
+    case TCU_BF16_F32 * 2 + 0: return launch_poly_one<TCU_BF16_F32, 16>(coef, n, pts, np, out, stream, num_cus);
+    case TCU_BF16_F32 * 2 + 1: return launch_poly_one<TCU_BF16_F32, 32>(coef, n, pts, np, out, stream, num_cus);
+    case TCU_BF16_BF16 * 2 + 0: return launch_poly_one<TCU_BF16_BF16, 16>(coef, n, pts, np, out, stream, num_cus);
+    case TCU_BF16_BF16 * 2 + 1: return launch_poly_one<TCU_BF16_BF16, 32>(coef, n, pts, np, out, stream, num_cus);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace tcu

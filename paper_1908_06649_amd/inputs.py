@@ -48,6 +48,13 @@ RECT_WORKLOADS = {
                                        N=8200, s=32, acc=False, dist="normal", seed=7),
 }
 
+# Workloads of batch polynomial evaluation (tcu_poly_eval, Theorem 11):
+# n coefficients ~ N(0,1) and p points ~ U[-1, 1), both in the input type.
+POLY_WORKLOADS = {
+    "poly_bf16_n4096_p16777216_s32": dict(kind="poly", dtype="bf16", out="f32", n=4096,
+                                          p=1 << 24, s=32, seed=8),
+}
+
 TORCH_DTYPE = {"f16": torch.float16, "bf16": torch.bfloat16, "i8": torch.int8,
                "f32": torch.float32, "i32": torch.int32}
 
@@ -89,6 +96,15 @@ def make_inputs(spec: dict, seed: int | None = None):
     A = draw(a_shape, spec["dtype"], spec["dist"], gen)
     B = draw(b_shape, spec["dtype"], spec["dist"], gen)
     return A, B
+
+
+def make_poly_inputs(spec: dict):
+    """(coefficients, points) of a polynomial workload: coefficients first."""
+    gen = torch.Generator(device="cpu")
+    gen.manual_seed(spec["seed"])
+    coef = draw((spec["n"],), spec["dtype"], "normal", gen)
+    pts = draw((spec["p"],), spec["dtype"], "uniform", gen)
+    return coef, pts
 
 
 def make_c0(spec: dict) -> torch.Tensor:

@@ -7,6 +7,8 @@ fallback: if ``libtcu.so`` is missing or fails to load, every call raises.
 
     tcu_mm_tall(A, n, s, B, C)   C (n x s) = A (n x s) @ B (s x s)     (native call)
     tcu_gemm(A, B, C, N)         C (N x N) = A @ B, unit size tcu_get_unit()
+    tcu_poly_eval(coef, n, points, p, out)
+                                 out[i] = sum_h coef[h] * points[i]**h    (Theorem 11)
     tcu_gemm_rect(A, lda, B, ldb, C, ldc, M, K, N, flags)
                                  C (M x N) = [C +] A (M x K) @ B (K x N); A, B and C
                                  may be row-strided 2-D views (row pitch = ld)
@@ -56,6 +58,8 @@ SIGNATURES = {
     "tcu_gemm_rect": (_int, [_vp, _i64, _vp, _i64, _vp, _i64, _i64, _i64, _i64, _int]),
     "tcu_gemm_rect_ex": (_int, [_vp, _i64, _vp, _i64, _vp, _i64, _i64, _i64, _i64, _int,
                                 _int, _int, _vp]),
+    "tcu_poly_eval": (_int, [_vp, _i64, _vp, _i64, _vp]),
+    "tcu_poly_eval_ex": (_int, [_vp, _i64, _vp, _i64, _vp, _int, _int, _vp]),
     "tcu_calls": (_i64, []),
     "tcu_square_calls": (_i64, []),
     "tcu_work": (_i64, []),
@@ -233,6 +237,42 @@ def tcu_gemm_rect_ex(A, lda: int, B, ldb: int, C, ldc: int, M: int, K: int, N: i
     st = _stream_ptr(dev) if stream_ptr is None else stream_ptr
     _check(lib().tcu_gemm_rect_ex(pa, int(lda), pb, int(ldb), pc, int(ldc), int(M), int(K),
                                   int(N), int(flags), int(s), dt, st), "tcu_gemm_rect_ex")
+
+
+def _poly_dtype(pts_dtype, out_dtype) -> int:
+    import torch
+    table = {(torch.float16, torch.float32): TCU_F16_F32,
+             (torch.bfloat16, torch.float32): TCU_BF16_F32,
+             (torch.bfloat16, torch.bfloat16): TCU_BF16_BF16}
+    try:
+        return table[(pts_dtype, out_dtype)]
+    except KeyError:
+        raise TcuError(TCU_ERR_UNSUPPORTED, f"dtype pair ({pts_dtype}, {out_dtype})") from None
+
+
+def tcu_poly_eval(coef, n: int, points, p: int, out) -> None:
+    """Theorem 11: out[i] = sum_{h<n} coef[h] * points[i]**h, unit size tcu_get_unit()."""
+    dt = _poly_dtype(points.dtype, out.dtype)
+    if coef.dtype != points.dtype:
+        raise ValueError("tcu_poly_eval: coefficients and points must share one input type")
+    dev, (ppts, pcoef, pout) = _marshal("tcu_poly_eval", (points, coef, out), (p, n, p))
+    L = lib()
+    _check(L.tcu_set_dtype(dt), "tcu_poly_eval")
+    _check(L.tcu_set_stream(_stream_ptr(dev)), "tcu_poly_eval")
+    _check(L.tcu_poly_eval(pcoef or None, int(n), ppts or None, int(p), pout or None),
+           "tcu_poly_eval")
+
+
+def tcu_poly_eval_ex(coef, n: int, points, p: int, out, s: int,
+                     stream_ptr: int | None = None) -> None:
+    """Stateless batch polynomial evaluation (unit size, dtype, stream as arguments)."""
+    dt = _poly_dtype(points.dtype, out.dtype)
+    if coef.dtype != points.dtype:
+        raise ValueError("tcu_poly_eval_ex: coefficients and points must share one input type")
+    dev, (ppts, pcoef, pout) = _marshal("tcu_poly_eval_ex", (points, coef, out), (p, n, p))
+    st = _stream_ptr(dev) if stream_ptr is None else stream_ptr
+    _check(lib().tcu_poly_eval_ex(pcoef or None, int(n), ppts or None, int(p), pout or None,
+                                  int(s), dt, st), "tcu_poly_eval_ex")
 
 
 # --------------------------------------------------------- cost accounting
