@@ -16,6 +16,9 @@ numpy in/out:
 * ``poly_eval(coef, points, dtype)`` -- A(x) = sum_h a_h x^h at every point
   (Theorem 11, Section 4.8), in binary64 on the decoded 16-bit inputs, with
   the magnitude sum sum_h |a_h| |x|^h.
+* ``transitive_closure(d)`` -- reachability by paths of >= 1 edge from an
+  n x n 0/1 adjacency matrix (Section 4.3), by the in-place iterative
+  algorithm the section starts from (k outermost, then i, then j).
 * ``mm_acc(A, B, C0, dtype, out)`` -- the accumulating form ``C0 + A*B``
   that the D functions of Sections 4.2 and 4.3 ask of the unit
   (X <- X + Y*Z); C0 holds stored output values ('f32', 'bf16' bits or
@@ -62,6 +65,8 @@ def _load():
     lib.oracle_mm_i64.restype = ctypes.c_int
     lib.oracle_poly_eval.argtypes = [ctypes.c_int, vp, i64, vp, i64, vp, vp]
     lib.oracle_poly_eval.restype = ctypes.c_int
+    lib.oracle_transitive_closure.argtypes = [vp, i64, vp]
+    lib.oracle_transitive_closure.restype = ctypes.c_int
     lib.oracle_threads.argtypes = []
     lib.oracle_threads.restype = ctypes.c_int
     _lib = lib
@@ -169,3 +174,15 @@ def poly_eval(coef: np.ndarray, points: np.ndarray, dtype: str):
     if rc != 0:
         raise ValueError("oracle rejected its arguments")
     return val, mag
+
+
+def transitive_closure(d: np.ndarray) -> np.ndarray:
+    """Closure of the n x n adjacency matrix d (nonzero = edge) as uint8 0/1."""
+    d = np.ascontiguousarray(d).view(np.uint8)
+    if d.ndim != 2 or d.shape[0] != d.shape[1]:
+        raise ValueError("adjacency matrix must be square")
+    out = np.empty_like(d)
+    rc = _load().oracle_transitive_closure(_ptr(d), d.shape[0], _ptr(out))
+    if rc != 0:
+        raise ValueError("oracle rejected its arguments")
+    return out

@@ -270,3 +270,41 @@ int oracle_poly_eval(int dtype, const void *coef, int64_t n, const void *pts, in
     free(a);
     return 0;
 }
+
+/* ---------------------------------------------------- transitive closure */
+/*
+ * Transitive closure of a directed graph (Section 4.3): from the n x n 0/1
+ * adjacency matrix d, c[i][j] = 1 iff j is reachable from i by a path of one
+ * or more edges.  The oracle is the iterative algorithm the section starts
+ * from, d[i][j] <- d[i][j] OR (d[i][k] AND d[k][j]) for k, then i, then j,
+ * updating d in place.  Rows are held as bit sets (bit j of row i), so the
+ * innermost j loop ORs row k into row i one 64-bit word at a time whenever
+ * d[i][k] = 1 -- the same loop order and the same updates.
+ *   d: n*n bytes, row-major, 0 = no edge, anything else = edge (read);
+ *   out: n*n bytes, the closure as 0/1 (written).
+ */
+int oracle_transitive_closure(const uint8_t *d, int64_t n, uint8_t *out)
+{
+    if (n < 0) return -1;
+    const int64_t words = (n + 63) / 64;
+    uint64_t *bits = (uint64_t *)calloc((size_t)(n > 0 ? n * words : 1), sizeof(uint64_t));
+    if (!bits) return -2;
+    for (int64_t i = 0; i < n; ++i)
+        for (int64_t j = 0; j < n; ++j)
+            if (d[i * n + j]) bits[i * words + j / 64] |= (uint64_t)1 << (j % 64);
+    for (int64_t k = 0; k < n; ++k) {
+        const uint64_t *rk = bits + k * words;
+        const uint64_t kbit = (uint64_t)1 << (k % 64);
+#pragma omp parallel for schedule(static)
+        for (int64_t i = 0; i < n; ++i) {
+            uint64_t *ri = bits + i * words;
+            if (ri[k / 64] & kbit)
+                for (int64_t w = 0; w < words; ++w) ri[w] |= rk[w];
+        }
+    }
+    for (int64_t i = 0; i < n; ++i)
+        for (int64_t j = 0; j < n; ++j)
+            out[i * n + j] = (uint8_t)((bits[i * words + j / 64] >> (j % 64)) & 1u);
+    free(bits);
+    return 0;
+}

@@ -107,6 +107,16 @@ def make_poly_inputs(spec: dict):
     return coef, pts
 
 
+def digraph(n: int, avg_out_degree: float, seed: int) -> torch.Tensor:
+    """Random directed graph as an n x n int8 0/1 adjacency matrix: each
+    ordered pair (i, j), self loops included, is an edge independently with
+    probability avg_out_degree / n."""
+    gen = torch.Generator(device="cpu")
+    gen.manual_seed(seed)
+    q = min(1.0, avg_out_degree / max(n, 1))
+    return (torch.rand((n, n), generator=gen) < q).to(torch.int8)
+
+
 def make_c0(spec: dict) -> torch.Tensor:
     """Initial output of an accumulating workload: standard normal in the
     output type (float32 or bfloat16), or int32 uniform in [-2^20, 2^20),

@@ -1,0 +1,125 @@
+"""Pins of the oracle's transitive closure (Section 4.3) against what the
+mathematics fixes (CPU only).
+
+The oracle is the in-place iterative algorithm (k, then i, then j).  It is
+checked against breadth-first search from every vertex (an independent
+algorithm), against invariants every closure satisfies (it contains the
+edges, is transitive, and is its own closure), against graphs with known
+closures (empty, path, cycle, complete, self loops, a DAG, disjoint cycles),
+and a group of plausible mistakes must fail the BFS pin.
+"""
+from collections import deque
+
+import numpy as np
+import pytest
+
+from paper_1908_06649_amd import inputs
+
+
+def bfs_closure(d: np.ndarray) -> np.ndarray:
+    """c[i][j] = 1 iff j is reachable from i by a path of >= 1 edge."""
+    n = d.shape[0]
+    adj = [np.nonzero(d[i])[0].tolist() for i in range(n)]
+    c = np.zeros((n, n), dtype=np.uint8)
+    for src in range(n):
+        seen = [False] * n
+        q = deque(adj[src])
+        for v in adj[src]:
+            seen[v] = True
+        while q:
+            u = q.popleft()
+            c[src, u] = 1
+            for v in adj[u]:
+                if not seen[v]:
+                    seen[v] = True
+                    q.append(v)
+    return c
+
+
+def graph(n, deg, seed):
+    return inputs.digraph(n, deg, seed).numpy().view(np.uint8)
+
+
+def bfs_pin(fn) -> bool:
+    for n, deg, seed in [(1, 1.0, 1), (2, 1.0, 2), (5, 1.5, 3), (17, 1.2, 4), (40, 0.9, 5),
+                         (64, 1.1, 6), (65, 2.0, 7), (130, 1.0, 8)]:
+        d = graph(n, deg, seed)
+        if not np.array_equal(fn(d), bfs_closure(d)):
+            return False
+    return True
+
+
+def test_tc_vs_bfs(oracle_mod):
+    assert bfs_pin(oracle_mod.transitive_closure)
+
+
+@pytest.mark.parametrize("deg", [0.5, 1.0, 1.5, 3.0, 20.0])
+def test_tc_vs_bfs_densities(oracle_mod, deg):
+    d = graph(97, deg, int(deg * 10))
+    assert np.array_equal(oracle_mod.transitive_closure(d), bfs_closure(d))
+
+
+def test_tc_invariants(oracle_mod):
+    d = graph(300, 1.05, 11)
+    c = oracle_mod.transitive_closure(d)
+    assert set(np.unique(c).tolist()) <= {0, 1}
+    assert np.all(c >= (d != 0))                               # contains every edge
+    ci = c.astype(np.int64)
+    assert np.all(((ci @ ci) > 0) <= (c > 0))                  # transitive
+    assert np.array_equal(oracle_mod.transitive_closure(c), c)  # idempotent
+
+
+def test_tc_known_graphs(oracle_mod):
+    n = 50
+    tc = oracle_mod.transitive_closure
+    assert not np.any(tc(np.zeros((n, n), np.uint8)))
+    path = np.eye(n, k=1, dtype=np.uint8)
+    assert np.array_equal(tc(path), np.triu(np.ones((n, n), np.uint8), 1))
+    cycle = np.roll(np.eye(n, dtype=np.uint8), 1, axis=1)
+    assert np.all(tc(cycle) == 1)
+    complete = (1 - np.eye(n, dtype=np.uint8)).astype(np.uint8)
+    assert np.all(tc(complete) == 1)                           # every vertex on a 2-cycle
+    loop = np.zeros((n, n), np.uint8)
+    loop[7, 7] = 1
+    c = tc(loop)
+    assert c[7, 7] == 1 and c.sum() == 1
+    dag = np.triu(graph(n, 5.0, 12), 1)
+    c = tc(dag)
+    assert not np.any(np.tril(c))                              # still acyclic
+    two = np.zeros((n, n), np.uint8)
+    for lo, hi in ((0, 20), (20, 50)):
+        idx = np.arange(lo, hi)
+        two[idx, np.roll(idx, 1)] = 1
+    c = tc(two)
+    assert np.all(c[:20, :20] == 1) and np.all(c[20:, 20:] == 1)
+    assert not np.any(c[:20, 20:]) and not np.any(c[20:, :20])
+
+
+def _mutants(oracle_mod):
+    def one_squaring(d):          # paths of length <= 2 only
+        di = (d != 0).astype(np.int64)
+        return ((di + di @ di) > 0).astype(np.uint8)
+
+    def reflexive(d):             # adds i -> i for every vertex
+        c = oracle_mod.transitive_closure(d).copy()
+        np.fill_diagonal(c, 1)
+        return c
+
+    def reversed_edges(d):
+        return oracle_mod.transitive_closure(np.ascontiguousarray(d.T))
+
+    def i_outer(d):               # loop order i, k, j instead of k, i, j
+        c = (d != 0).astype(np.uint8)
+        n = c.shape[0]
+        for i in range(n):
+            for k in range(n):
+                if c[i, k]:
+                    c[i] |= c[k]
+        return c
+
+    return [one_squaring, reflexive, reversed_edges, i_outer]
+
+
+def test_tc_pin_catches_planted_mistakes(oracle_mod):
+    for mut in _mutants(oracle_mod):
+        assert not bfs_pin(mut), mut.__name__
