@@ -19,6 +19,10 @@ JSON line:
   poly       batch polynomial evaluation (tcu_poly_eval, Theorem 11) on 2^24
              points with 4096 coefficients: TFLOP/s of the method's 2pn
              multiply-adds vs the bf16 matrix-core peak
+  tc         transitive closure (tcu_transitive_closure, Theorem 5) of a
+             random 8192-vertex digraph: GB/s of the D updates' algorithmic
+             traffic (each pivot band reads and writes the off-band n^2 bytes)
+             vs HBM peak, and boolean TOP/s (2 n^3 / t)
   rect       the rectangular / accumulating product (tcu_gemm_rect):
              Corollary 1's sqrt(n) x r by r x sqrt(n) with r below and above
              sqrt(n), accumulating into C, and an order-8200 product that
@@ -59,9 +63,9 @@ PROFILES = os.path.join(ROOT, "profiles")
 
 
 def kernel_sources(kind: str):
-    main = {"gemm": "tcu_gemm.hip", "rect": "tcu_gemm.hip", "poly": "tcu_poly.hip"}.get(
-        kind, "tcu_tall.hip")
-    return [os.path.join(CSRC, f) for f in (main, "tcu_device.h")]
+    main = {"gemm": ["tcu_gemm.hip"], "rect": ["tcu_gemm.hip"], "poly": ["tcu_poly.hip"],
+            "tc": ["tcu_tc.hip", "tcu_gemm.hip"]}.get(kind, ["tcu_tall.hip"])
+    return [os.path.join(CSRC, f) for f in (*main, "tcu_device.h")]
 
 
 def kernel_hash(kind: str) -> str:
@@ -95,12 +99,21 @@ def counted_traffic(name: str, kind: str):
 def algorithmic(spec: dict):
     """(work per call in flop/op, bytes per call) that the method must do."""
     from paper_1908_06649_amd import inputs
-    ib = 1 if spec["dtype"] == "i8" else 2
-    ob = 2 if spec["out"] == "bf16" else 4
+    ib = 1 if spec.get("dtype", "i8") == "i8" else 2
+    ob = 2 if spec.get("out") == "bf16" else 4
     if spec["kind"] == "tall":
         n, s = spec["n"], spec["s"]
         return 2.0 * n * s * s, n * s * ib + s * s * ib + n * s * ob
     del inputs
+    if spec["kind"] == "tc":
+        # per pivot band of up to 256 vertices: the D update reads and writes
+        # every off-band entry once, the panel updates their band entries
+        n = spec["n"]
+        nbytes = 0
+        for k0 in range(0, n, 256):
+            bk = min(256, n - k0)
+            nbytes += 2 * (n - bk) ** 2 + 2 * 2 * bk * (n - bk) + 2 * bk * bk
+        return 2.0 * n ** 3, nbytes + 2 * n * n          # + the normalizing pass
     if spec["kind"] == "poly":
         n, p = spec["n"], spec["p"]
         return 2.0 * n * p, n * ib + p * ib + p * ob
@@ -120,9 +133,15 @@ class Workload:
         from paper_1908_06649_amd import inputs, tcu
         self.name = name
         self.spec = (inputs.WORKLOADS.get(name) or inputs.RECT_WORKLOADS.get(name)
-                     or inputs.POLY_WORKLOADS[name])
+                     or inputs.POLY_WORKLOADS.get(name) or inputs.TC_WORKLOADS[name])
         self.tcu = tcu
         self.s = self.spec["s"]
+        if self.spec["kind"] == "tc":
+            # the closure is computed in place; the algorithm's work does not
+            # depend on the data, so repeated calls on the same array time it
+            self.A = inputs.make_tc_input(self.spec)
+            self.dA = self.A.cuda()
+            return
         if self.spec["kind"] == "poly":
             self.A, self.B = inputs.make_poly_inputs(self.spec)     # coefficients, points
             self.dA, self.dB = self.A.cuda(), self.B.cuda()
@@ -143,6 +162,8 @@ class Workload:
         sp = self.spec
         if sp["kind"] == "gemm":
             self.tcu.tcu_gemm(self.dA, self.dB, self.C, sp["N"])
+        elif sp["kind"] == "tc":
+            self.tcu.tcu_transitive_closure(self.dA, sp["n"], sp["n"])
         elif sp["kind"] == "poly":
             self.tcu.tcu_poly_eval(self.dA, sp["n"], self.dB, sp["p"], self.C)
         elif sp["kind"] == "rect":
@@ -203,7 +224,16 @@ def measure(name: str, steps: int, warmup: int) -> dict:
     kind = sp["kind"]
     out = {"workload": name, "ms_per_call": ms, "calls": calls, "square_calls": squares,
            "model_work": work}
-    if kind in ("gemm", "rect", "poly"):
+    if kind == "tc":
+        gbs = nbytes / (ms * 1e-3) / 1e9
+        out.update({"value": gbs, "unit": "GB/s",
+                    "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS,
+                                 "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS,
+                                 "traffic": counted_traffic(name, kind)},
+                    "bool_tops": flops / (ms * 1e-3) / 1e12,
+                    "algorithmic_bytes": nbytes,
+                    "calls_section43": (-(-sp["n"] // sp["s"])) * (-(-sp["n"] // sp["s"]) - 1)})
+    elif kind in ("gemm", "rect", "poly"):
         tput = flops / (ms * 1e-3) / 1e12
         peak = PEAK[sp["dtype"]]
         out.update({"value": tput, "unit": "TOP/s" if sp["dtype"] == "i8" else "TFLOP/s",
@@ -315,6 +345,7 @@ def main() -> int:
     ap.add_argument("--workload", default=HEADLINE)
     ap.add_argument("--no-rect", action="store_true")
     ap.add_argument("--no-poly", action="store_true")
+    ap.add_argument("--no-tc", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--copy-probe", action="store_true")
@@ -334,7 +365,8 @@ def main() -> int:
     if args.copy_probe:
         copy_probe()
         return 0
-    known = {**inputs.WORKLOADS, **inputs.RECT_WORKLOADS, **inputs.POLY_WORKLOADS}
+    known = {**inputs.WORKLOADS, **inputs.RECT_WORKLOADS, **inputs.POLY_WORKLOADS,
+             **inputs.TC_WORKLOADS}
     if args.workload not in known:
         names = sorted(known)
         print(f"unknown workload {args.workload}; choose from {names}", file=sys.stderr)
@@ -354,12 +386,14 @@ def main() -> int:
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": sp["dtype"],
+        "dtype": sp.get("dtype", "u8"),
         "data": "synthetic (seeded i.i.d. matrices; the paper has no datasets)",
         "config": {"workload": args.workload,
-                   **{k: sp[k] for k in ("kind", "M", "K", "N", "n", "p", "s", "acc") if k in sp},
-                   "dtype_in": sp["dtype"], "dtype_out": sp["out"],
-                   "distribution": sp.get("dist", "coefficients N(0,1), points U[-1,1)"),
+                   **{k: sp[k] for k in ("kind", "M", "K", "N", "n", "p", "s", "acc", "deg")
+                      if k in sp},
+                   "dtype_in": sp.get("dtype", "u8"), "dtype_out": sp.get("out", "u8"),
+                   "distribution": sp.get("dist", "coefficients N(0,1), points U[-1,1)"
+                                          if sp["kind"] == "poly" else "random digraph"),
                    "seed": sp["seed"]},
         "roofline": main_res["roofline"],
     }
@@ -412,9 +446,21 @@ def main() -> int:
                                             "model_work")}
             torch.cuda.empty_cache()
         result["poly"] = poly
+    if not args.no_tc:
+        tc = {}
+        for name in inputs.TC_WORKLOADS:
+            if name == args.workload:
+                continue
+            r = measure(name, args.steps, max(args.warmup, 5))
+            r.pop("_workload")
+            tc[name] = {k: r[k] for k in ("value", "unit", "ms_per_call", "roofline", "bool_tops",
+                                          "calls", "calls_section43", "square_calls",
+                                          "model_work")}
+            torch.cuda.empty_cache()
+        result["tc"] = tc
     result["cost_model"] = cost
     result["kernel_source_sha256"] = {"gemm": kernel_hash("gemm"), "tall": kernel_hash("tall"),
-                                      "poly": kernel_hash("poly")}
+                                      "poly": kernel_hash("poly"), "tc": kernel_hash("tc")}
     print(json.dumps(result), flush=True)
     return 0
 

@@ -15,6 +15,7 @@
  *     B into s x s blocks B_{i,j}, and output strip j is sum_i A_i * B_{i,j}.
  *   - tcu_gemm_rect: the same decomposition for rectangular, strided and
  *     accumulating products (Corollary 1; the D functions' update).
+ *   - tcu_transitive_closure: the blocked transitive closure (Theorem 5).
  *   - tcu_poly_eval: batch polynomial evaluation (Theorem 11).
  *
  * Throughout, s = sqrt(m) is the unit size (a machine parameter of the
@@ -222,6 +223,29 @@ int tcu_gemm_rect_ex(const void *A, int64_t lda, const void *B, int64_t ldb, voi
 int tcu_poly_eval(const void *coef, int64_t n, const void *points, int64_t p, void *out);
 int tcu_poly_eval_ex(const void *coef, int64_t n, const void *points, int64_t p, void *out, int s,
                      int dtype, void *hip_stream);
+
+/* ---- transitive closure (Theorem 5, Section 4.3) ----
+ *
+ * X <- the transitive closure of the directed graph whose n x n adjacency
+ * matrix X holds: afterwards X[i][j] = 1 iff vertex j is reachable from
+ * vertex i by a path of one or more edges, else 0.  In place.
+ *   X: n x n int8 entries, row i at X + i*ld bytes (ld >= n); on input any
+ *      nonzero byte is an edge (self loops allowed); on output 0 or 1.
+ *   n: number of vertices, 0 <= n <= TCU_MAX_RECT_DIM (n = 0 is a no-op);
+ *      need not be a multiple of s.
+ * The section's blocked algorithm: per pivot block, close the diagonal
+ * block (A), update the pivot block row and column through it (B, C), then
+ * every other block by the D function X_ij <- min(X_ij + X_ik X_kj, 1) on the
+ * int8 matrix cores.  Pivot blocks here are 256 vertices wide.
+ * The unit size comes from tcu_get_unit() (it sets the cost accounting);
+ * the stream from tcu_get_stream().  Errors: TCU_ERR_NULL, TCU_ERR_SHAPE
+ * (n out of range, ld < n, extent of 2^40 bytes or more),
+ * TCU_ERR_UNSUPPORTED, TCU_ERR_ALIGN (X not 16-byte aligned),
+ * TCU_ERR_NO_DEVICE, TCU_ERR_HIP.
+ * Cost accounting (the s-blocked algorithm): q(q-1) calls of the D function
+ * with q = ceil(n/s), each of (q-1) square calls. */
+int tcu_transitive_closure(void *X, int64_t n, int64_t ld);
+int tcu_transitive_closure_ex(void *X, int64_t n, int64_t ld, int s, void *hip_stream);
 
 /* ---- cost accounting (Theorem 2 proof; Section 5 weak model) ----
  * tcu_calls:        logical tensor-unit calls issued (1 per tall call,

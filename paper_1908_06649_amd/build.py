@@ -14,7 +14,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libtcu.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
-SOURCES = ["tcu_abi.cpp", "tcu_tall.hip", "tcu_gemm.hip", "tcu_poly.hip"]
+SOURCES = ["tcu_abi.cpp", "tcu_tall.hip", "tcu_gemm.hip", "tcu_poly.hip", "tcu_tc.hip"]
 ARCH = "gfx950"
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden",

@@ -179,6 +179,15 @@ int validate_poly(const void *coef, int64_t n, const void *pts, int64_t p, const
   return TCU_OK;
 }
 
+int validate_tc(const void *X, int64_t n, int64_t ld, int s) {
+  if (!unit_ok(s)) return TCU_ERR_UNSUPPORTED;
+  if (n < 0 || n > TCU_MAX_RECT_DIM || ld < n) return TCU_ERR_SHAPE;
+  if (!X && n > 0) return TCU_ERR_NULL;
+  if (n > 0 && view_extent(n, n, ld, 1) >= ((int64_t)1 << 40)) return TCU_ERR_SHAPE;
+  if (misaligned(X)) return TCU_ERR_ALIGN;
+  return TCU_OK;
+}
+
 }  // namespace
 
 TCU_EXPORT int tcu_set_unit(int s) {
@@ -301,6 +310,32 @@ TCU_EXPORT int tcu_poly_eval_ex(const void *coef, int64_t n, const void *points,
 TCU_EXPORT int tcu_poly_eval(const void *coef, int64_t n, const void *points, int64_t p,
                              void *out) {
   return tcu_poly_eval_ex(coef, n, points, p, out, g_cfg.s, g_cfg.dtype, g_cfg.stream);
+}
+
+TCU_EXPORT int tcu_transitive_closure_ex(void *X, int64_t n, int64_t ld, int s,
+                                         void *hip_stream) {
+  int rc = validate_tc(X, n, ld, s);
+  if (rc != TCU_OK) return rc;
+  if (n == 0) return TCU_OK;
+  int num_cus = 0;
+  rc = device_ready(&num_cus);
+  if (rc != TCU_OK) return rc;
+  if (tcu::launch_tc((unsigned char *)X, ld, n, (hipStream_t)hip_stream, num_cus) != hipSuccess)
+    return TCU_ERR_HIP;
+  // The section's blocked algorithm with s-wide blocks: for each of the
+  // q = ceil(n/s) pivots, q - 1 tall calls of the D function (pivot row
+  // block X_kj as the weights, the (q - 1) s rows of the other X_ik
+  // streamed through).
+  const int64_t q = (n + s - 1) / s;
+  const int64_t calls = q * (q - 1);
+  g_calls.fetch_add(calls, std::memory_order_relaxed);
+  g_square_calls.fetch_add(calls * (q - 1), std::memory_order_relaxed);
+  g_work.fetch_add(calls * (q - 1) * s * s, std::memory_order_relaxed);
+  return TCU_OK;
+}
+
+TCU_EXPORT int tcu_transitive_closure(void *X, int64_t n, int64_t ld) {
+  return tcu_transitive_closure_ex(X, n, ld, g_cfg.s, g_cfg.stream);
 }
 
 TCU_EXPORT int64_t tcu_calls(void) { return g_calls.load(std::memory_order_relaxed); }

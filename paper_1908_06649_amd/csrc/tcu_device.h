@@ -18,10 +18,19 @@ typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 
+// Internal element-type code: int8 0/1 inputs, int8 0/1 output formed as
+// old OR (sum > 0) -- the update X <- min(X + Y Z, 1) of the transitive
+// closure's D function on 0/1 matrices.  Not part of the public tcu_dtype.
+constexpr int TCU_I8_BOOL = 16;
+
 // Input element size in bytes for a tcu_dtype.
-__host__ __device__ constexpr int in_bytes(int dt) { return dt == TCU_I8_I32 ? 1 : 2; }
+__host__ __device__ constexpr int in_bytes(int dt) {
+  return (dt == TCU_I8_I32 || dt == TCU_I8_BOOL) ? 1 : 2;
+}
 // Output element size in bytes for a tcu_dtype.
-__host__ __device__ constexpr int out_bytes(int dt) { return dt == TCU_BF16_BF16 ? 2 : 4; }
+__host__ __device__ constexpr int out_bytes(int dt) {
+  return dt == TCU_BF16_BF16 ? 2 : dt == TCU_I8_BOOL ? 1 : 4;
+}
 
 template <typename T, typename S>
 __device__ __forceinline__ T bitcast(const S &s) {
@@ -163,7 +172,21 @@ __device__ __forceinline__ u32x4 load_chunk(const unsigned char *p, int valid) {
 // access of the 4 values.
 template <int DT, bool kVec, typename Acc>
 __device__ __forceinline__ void store_out4(unsigned char *p, Acc v, int valid, bool acc) {
-  if constexpr (DT == TCU_BF16_BF16) {
+  if constexpr (DT == TCU_I8_BOOL) {
+    // 0/1 output: old OR (sum > 0); the accumulate flag is implied.
+    if (kVec && valid >= 4) {
+      const unsigned old = *(const unsigned *)p;
+      unsigned w = 0;
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        w |= (unsigned)((((old >> (8 * e)) & 0xffu) != 0u) | (v[e] > 0)) << (8 * e);
+      *(unsigned *)p = w;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (e < valid) p[e] = (unsigned char)((p[e] != 0) | (v[e] > 0));
+    }
+  } else if constexpr (DT == TCU_BF16_BF16) {
     unsigned short *q = (unsigned short *)p;
     if (kVec && valid >= 4) {
       if (acc) {

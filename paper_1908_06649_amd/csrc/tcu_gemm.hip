@@ -47,6 +47,7 @@ namespace {
 #endif
 
 constexpr int kBKB = 128;  // bytes of the contracted index per K-step and LDS row
+constexpr int kNoBand = 0x7fffffff;
 
 __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row ^ (row >> 3)) & 7); }
 
@@ -82,8 +83,9 @@ __global__ __attribute__((amdgpu_flat_work_group_size(64 * WM * WN, 64 * WM * WN
                           amdgpu_waves_per_eu(1, 1))) void
 gemm_kernel(const unsigned char *__restrict__ A, const unsigned char *__restrict__ B,
             unsigned char *__restrict__ C, int M, int N, int K, int64_t lda, int64_t ldb,
-            int64_t ldc, int accum, int tiles_m, int tiles_n) {
-  constexpr bool kI8 = (DT == TCU_I8_I32);
+            int64_t ldc, int accum, int tiles_m, int tiles_n, int band_tm, int skip_m,
+            int band_tn, int skip_n) {
+  constexpr bool kI8 = (in_bytes(DT) == 1);
   constexpr int NT = 64 * WM * WN;
   constexpr int ES = in_bytes(DT);
   constexpr int OB = out_bytes(DT);
@@ -104,7 +106,11 @@ gemm_kernel(const unsigned char *__restrict__ A, const unsigned char *__restrict
 
   int tm, tn;
   map_tile(blockIdx.x, tiles_m, tiles_n, tm, tn);
-  const int m0 = tm * BM, n0 = tn * BN;
+  // Tile rows from band_tm on (columns from band_tn on) start skip_m
+  // (skip_n) further: the tiles then step over a band of the output that
+  // another launch owns (the transitive closure's pivot block row/column).
+  const int m0 = tm * BM + (tm >= band_tm ? skip_m : 0);
+  const int n0 = tn * BN + (tn >= band_tn ? skip_n : 0);
   const int64_t lda_b = lda * ES, ldb_b = ldb * ES, ldc_b = ldc * OB;  // row pitches in bytes
 
   const int tid = threadIdx.x;
@@ -566,7 +572,27 @@ hipError_t launch_cfg(const RectArgs &a, hipStream_t stream) {
   hipLaunchKernelGGL((gemm_kernel<DT, BM, BN, WM, WN, kVec>), dim3(tiles_m * tiles_n),
                      dim3(64 * WM * WN), 0, stream, (const unsigned char *)a.A,
                      (const unsigned char *)a.B, (unsigned char *)a.C, (int)a.M, (int)a.N,
-                     (int)a.K, a.lda, a.ldb, a.ldc, a.accum ? 1 : 0, tiles_m, tiles_n);
+                     (int)a.K, a.lda, a.ldb, a.ldc, a.accum ? 1 : 0, tiles_m, tiles_n,
+                     kNoBand, 0, kNoBand, 0);
+  return hipGetLastError();
+}
+
+// Boolean rank-Bk update of the transitive closure on 0/1 int8 data:
+// C[rows, cols] <- C OR (A[rows, 0:Bk] B[0:Bk, cols] > 0), the tile grid
+// skipping the pivot band [k0, k0 + Bk) in rows and/or columns.
+// rows_skip / cols_skip: whether the row / column range of C steps over the
+// band (then M / N is the matrix order n and the band starts at k0).
+template <int BM, int BN, bool kVec>
+hipError_t launch_bool(const unsigned char *A, const unsigned char *B, unsigned char *C,
+                       int64_t ld, int M, int N, int Bk, int k0, bool rows_skip, bool cols_skip,
+                       hipStream_t stream) {
+  const int rows = rows_skip ? M - Bk : M, cols = cols_skip ? N - Bk : N;
+  const int tiles_m = (rows + BM - 1) / BM, tiles_n = (cols + BN - 1) / BN;
+  if (tiles_m <= 0 || tiles_n <= 0) return hipSuccess;
+  hipLaunchKernelGGL((gemm_kernel<TCU_I8_BOOL, BM, BN, 2, 2, kVec>), dim3(tiles_m * tiles_n),
+                     dim3(256), 0, stream, A, B, C, M, N, Bk, ld, ld, ld, 1, tiles_m, tiles_n,
+                     rows_skip ? k0 / BM : kNoBand, rows_skip ? Bk : 0,
+                     cols_skip ? k0 / BN : kNoBand, cols_skip ? Bk : 0);
   return hipGetLastError();
 }
 
@@ -645,6 +671,40 @@ hipError_t launch_dt(const RectArgs &a, hipStream_t stream, int num_cus) {
 }
 
 }  // namespace
+
+hipError_t launch_tc_panels(unsigned char *X, int64_t ld, int n, int k0, int Bk,
+                            hipStream_t stream) {
+  // Pivot row band X[k0:k0+Bk, J] |= Y X[k0:k0+Bk, J] and pivot column band
+  // X[I, k0:k0+Bk] |= X[I, k0:k0+Bk] Y for J, I outside the band, Y the closed
+  // diagonal block.  Each tile spans the whole band (256 rows, resp.
+  // columns), so it reads exactly the band elements it rewrites and no other
+  // tile touches them.
+  unsigned char *band_row = X + (int64_t)k0 * ld;
+  unsigned char *band_col = X + k0;
+  const unsigned char *Y = X + (int64_t)k0 * ld + k0;
+  const bool vec = ld % 16 == 0;
+  hipError_t e;
+  if (vec) {
+    e = launch_bool<256, 64, true>(Y, band_row, band_row, ld, Bk, n, Bk, k0, false, true, stream);
+    if (e != hipSuccess) return e;
+    return launch_bool<64, 256, true>(band_col, Y, band_col, ld, n, Bk, Bk, k0, true, false,
+                                      stream);
+  }
+  e = launch_bool<256, 64, false>(Y, band_row, band_row, ld, Bk, n, Bk, k0, false, true, stream);
+  if (e != hipSuccess) return e;
+  return launch_bool<64, 256, false>(band_col, Y, band_col, ld, n, Bk, Bk, k0, true, false,
+                                     stream);
+}
+
+hipError_t launch_tc_rest(unsigned char *X, int64_t ld, int n, int k0, int Bk,
+                          hipStream_t stream) {
+  // X[I, J] |= X[I, k0:k0+Bk] X[k0:k0+Bk, J] for I, J outside the band: the
+  // D function, with x and + on the matrix cores and min(., 1) on the way out.
+  const unsigned char *L = X + k0;
+  const unsigned char *R = X + (int64_t)k0 * ld;
+  if (ld % 16 == 0) return launch_bool<128, 128, true>(L, R, X, ld, n, n, Bk, k0, true, true, stream);
+  return launch_bool<128, 128, false>(L, R, X, ld, n, n, Bk, k0, true, true, stream);
+}
 
 hipError_t launch_rect(int dtype, int s, const RectArgs &a, hipStream_t stream, int num_cus) {
   // A single contiguous strip times a single block is one native call.

@@ -27,6 +27,16 @@ struct RectArgs {
 };
 hipError_t launch_rect(int dtype, int s, const RectArgs &args, hipStream_t stream, int num_cus);
 
+// Transitive closure, in place on an n x n int8 0/1 matrix X with row pitch
+// ld: all pivot bands of Bk <= 256 vertices in order (see tcu_tc.hip).
+hipError_t launch_tc(unsigned char *X, int64_t ld, int64_t n, hipStream_t stream, int num_cus);
+// Its matrix-core phases for the band [k0, k0 + Bk): the pivot row and column
+// bands, then the rest of the matrix (tcu_gemm.hip).
+hipError_t launch_tc_panels(unsigned char *X, int64_t ld, int n, int k0, int Bk,
+                            hipStream_t stream);
+hipError_t launch_tc_rest(unsigned char *X, int64_t ld, int n, int k0, int Bk,
+                          hipStream_t stream);
+
 // Batch polynomial evaluation: out[i] = sum_{h<n} coef[h] * pts[i]^h for
 // i < np, 16-bit inputs (dtype TCU_F16_F32, TCU_BF16_F32 or TCU_BF16_BF16).
 hipError_t launch_poly(int dtype, int s, const void *coef, int64_t n, const void *pts, int64_t np,

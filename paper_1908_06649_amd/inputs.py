@@ -55,6 +55,13 @@ POLY_WORKLOADS = {
                                           p=1 << 24, s=32, seed=8),
 }
 
+# Workloads of the transitive closure (tcu_transitive_closure, Theorem 5):
+# a random digraph of n vertices, each ordered pair an edge with probability
+# deg / n (mean out-degree deg).
+TC_WORKLOADS = {
+    "tc_n8192_deg2": dict(kind="tc", n=8192, deg=2.0, s=32, seed=9),
+}
+
 TORCH_DTYPE = {"f16": torch.float16, "bf16": torch.bfloat16, "i8": torch.int8,
                "f32": torch.float32, "i32": torch.int32}
 
@@ -115,6 +122,11 @@ def digraph(n: int, avg_out_degree: float, seed: int) -> torch.Tensor:
     gen.manual_seed(seed)
     q = min(1.0, avg_out_degree / max(n, 1))
     return (torch.rand((n, n), generator=gen) < q).to(torch.int8)
+
+
+def make_tc_input(spec: dict) -> torch.Tensor:
+    """Adjacency matrix (int8 0/1) of a transitive-closure workload."""
+    return digraph(spec["n"], spec["deg"], spec["seed"])
 
 
 def make_c0(spec: dict) -> torch.Tensor:

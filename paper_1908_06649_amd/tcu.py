@@ -7,6 +7,7 @@ fallback: if ``libtcu.so`` is missing or fails to load, every call raises.
 
     tcu_mm_tall(A, n, s, B, C)   C (n x s) = A (n x s) @ B (s x s)     (native call)
     tcu_gemm(A, B, C, N)         C (N x N) = A @ B, unit size tcu_get_unit()
+    tcu_transitive_closure(X, n, ld)   X <- transitive closure, in place (Theorem 5)
     tcu_poly_eval(coef, n, points, p, out)
                                  out[i] = sum_h coef[h] * points[i]**h    (Theorem 11)
     tcu_gemm_rect(A, lda, B, ldb, C, ldc, M, K, N, flags)
@@ -60,6 +61,8 @@ SIGNATURES = {
                                 _int, _int, _vp]),
     "tcu_poly_eval": (_int, [_vp, _i64, _vp, _i64, _vp]),
     "tcu_poly_eval_ex": (_int, [_vp, _i64, _vp, _i64, _vp, _int, _int, _vp]),
+    "tcu_transitive_closure": (_int, [_vp, _i64, _i64]),
+    "tcu_transitive_closure_ex": (_int, [_vp, _i64, _i64, _int, _vp]),
     "tcu_calls": (_i64, []),
     "tcu_square_calls": (_i64, []),
     "tcu_work": (_i64, []),
@@ -273,6 +276,29 @@ def tcu_poly_eval_ex(coef, n: int, points, p: int, out, s: int,
     st = _stream_ptr(dev) if stream_ptr is None else stream_ptr
     _check(lib().tcu_poly_eval_ex(pcoef or None, int(n), ppts or None, int(p), pout or None,
                                   int(s), dt, st), "tcu_poly_eval_ex")
+
+
+def tcu_transitive_closure(X, n: int, ld: int) -> None:
+    """Theorem 5, in place: X (an n x n int8 view with row pitch ld) becomes
+    the transitive closure of the graph it is the adjacency matrix of."""
+    import torch
+    if X.dtype not in (torch.int8, torch.uint8):
+        raise ValueError("tcu_transitive_closure: X must be int8 or uint8")
+    dev, (px,) = _marshal_views("tcu_transitive_closure", ((X, n, n, ld),))
+    L = lib()
+    _check(L.tcu_set_stream(_stream_ptr(dev)), "tcu_transitive_closure")
+    _check(L.tcu_transitive_closure(px or None, int(n), int(ld)), "tcu_transitive_closure")
+
+
+def tcu_transitive_closure_ex(X, n: int, ld: int, s: int, stream_ptr: int | None = None) -> None:
+    """Stateless transitive closure (unit size and stream as arguments)."""
+    import torch
+    if X.dtype not in (torch.int8, torch.uint8):
+        raise ValueError("tcu_transitive_closure_ex: X must be int8 or uint8")
+    dev, (px,) = _marshal_views("tcu_transitive_closure_ex", ((X, n, n, ld),))
+    st = _stream_ptr(dev) if stream_ptr is None else stream_ptr
+    _check(lib().tcu_transitive_closure_ex(px or None, int(n), int(ld), int(s), st),
+           "tcu_transitive_closure_ex")
 
 
 # --------------------------------------------------------- cost accounting
