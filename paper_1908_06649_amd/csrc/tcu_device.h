@@ -244,7 +244,8 @@ __device__ __forceinline__ void store_out4(unsigned char *p, Acc v, int valid, b
 // which must be rounded once from the whole sum.
 template <int DT, typename Acc>
 __device__ __forceinline__ void atomic_add_out4(unsigned char *p, Acc v) {
-  static_assert(DT != TCU_BF16_BF16, "bfloat16 outputs are never split");
+  static_assert(DT == TCU_F16_F32 || DT == TCU_BF16_F32 || DT == TCU_I8_I32,
+                "only binary32 and int32 outputs are split");
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
     if constexpr (DT == TCU_I8_I32)

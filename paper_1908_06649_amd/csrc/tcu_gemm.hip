@@ -47,7 +47,7 @@ namespace {
 #endif
 
 constexpr int kBKB = 128;  // bytes of the contracted index per K-step and LDS row
-constexpr int kNoBand = 0x7fffffff;
+
 
 __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row ^ (row >> 3)) & 7); }
 
@@ -351,8 +351,8 @@ template <int DT, int kRing>
 __global__ __attribute__((amdgpu_flat_work_group_size(512, 512), amdgpu_waves_per_eu(2, 2))) void
 gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restrict__ B,
                unsigned char *__restrict__ C, int K, int64_t lda, int64_t ldb, int64_t ldc,
-               int accum, int tiles_m, int tiles_n, int nsplit) {
-  constexpr bool kI8 = (DT == TCU_I8_I32);
+               int accum, int tiles_m, int tiles_n, int nsplit, TileRemap remap) {
+  constexpr bool kI8 = (in_bytes(DT) == 1);
   constexpr int ES = in_bytes(DT);
   constexpr int OB = out_bytes(DT);
   constexpr int KE = kFastKB / ES;     // contracted elements per stage
@@ -388,8 +388,8 @@ gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restr
     const int slice = w / tiles;
     int tm, tn;
     map_tile(w - slice * tiles, tiles_m, tiles_n, tm, tn);
-    m0 = tm * 256;
-    n0 = tn * 256;
+    m0 = remap.m_base + tm * 256 + (tm >= remap.band_m ? remap.skip_m : 0);
+    n0 = remap.n_base + tn * 256 + (tn >= remap.band_n ? remap.skip_n : 0);
     const int s_begin = (int)((int64_t)nk_all * slice / nsplit);
     nk = (int)((int64_t)nk_all * (slice + 1) / nsplit) - s_begin;
     gbase = grp == 0 ? A + (int64_t)m0 * lda_b + (int64_t)s_begin * kFastKB
@@ -526,21 +526,59 @@ gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restr
       }
     }
 
-    // Epilogue: lane holds C[row][col .. col+3] of every accumulator block.
+    if constexpr (DT == TCU_I8_BOOL) {
+      // 0/1 output (a quarter of the bytes of a binary32 tile): the flags
+      // (sum > 0) go through LDS -- the ring is free after the loop's last
+      // barrier -- so that the read-modify-write of C is done in whole
+      // 16-byte row chunks, consecutive threads on consecutive chunks.
+      // Row stride 272 bytes: the 16 rows one store instruction touches
+      // land in distinct banks.
+      constexpr int kStride = 272;
+      unsigned char *stage = sA;
 #pragma unroll
-    for (int fn = 0; fn < FN; ++fn) {
+      for (int fn = 0; fn < FN; ++fn) {
 #pragma unroll
-      for (int fm = 0; fm < FM; ++fm) {
-        const int row = m0 + grp * 128 + fm * 16 + r;
-        const int col = n0 + q * 64 + fn * 16 + 4 * g;
-        unsigned char *p = C + (int64_t)row * ldc_b + (int64_t)col * OB;
-        if constexpr (DT != TCU_BF16_BF16) {
-          if (nsplit > 1) {
-            atomic_add_out4<DT>(p, acc[fn][fm]);
-            continue;
-          }
+        for (int fm = 0; fm < FM; ++fm) {
+          const int row = grp * 128 + fm * 16 + r;
+          const int col = q * 64 + fn * 16 + 4 * g;
+          unsigned w = 0;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) w |= (unsigned)(acc[fn][fm][e] > 0) << (8 * e);
+          *(unsigned *)(stage + row * kStride + col) = w;
         }
-        store_out4<DT, true>(p, acc[fn][fm], 4, accum != 0);
+      }
+      __syncthreads();
+      constexpr int kChunks = 256 * 16 / 512;   // 16-byte chunks per thread
+      u32x4 old[kChunks];
+#pragma unroll
+      for (int j = 0; j < kChunks; ++j) {
+        const int c = threadIdx.x + 512 * j, row = c >> 4, cc = c & 15;
+        old[j] = *(const u32x4 *)(C + (int64_t)(m0 + row) * ldc_b + n0 + 16 * cc);
+      }
+#pragma unroll
+      for (int j = 0; j < kChunks; ++j) {
+        const int c = threadIdx.x + 512 * j, row = c >> 4, cc = c & 15;
+        const u32x4 f = *(const u32x4 *)(stage + row * kStride + 16 * cc);
+        *(u32x4 *)(C + (int64_t)(m0 + row) * ldc_b + n0 + 16 * cc) = old[j] | f;
+      }
+      __syncthreads();   // staging reads done before the ring is refilled
+    } else {
+      // Epilogue: lane holds C[row][col .. col+3] of every accumulator block.
+#pragma unroll
+      for (int fn = 0; fn < FN; ++fn) {
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm) {
+          const int row = m0 + grp * 128 + fm * 16 + r;
+          const int col = n0 + q * 64 + fn * 16 + 4 * g;
+          unsigned char *p = C + (int64_t)row * ldc_b + (int64_t)col * OB;
+          if constexpr (DT == TCU_F16_F32 || DT == TCU_BF16_F32 || DT == TCU_I8_I32) {
+            if (nsplit > 1) {
+              atomic_add_out4<DT>(p, acc[fn][fm]);
+              continue;
+            }
+          }
+          store_out4<DT, true>(p, acc[fn][fm], 4, accum != 0);
+        }
       }
     }
     // Every wave finished reading the ring at the last barrier of the loop.
@@ -658,7 +696,7 @@ hipError_t launch_dt(const RectArgs &a, hipStream_t stream, int num_cus) {
     hipLaunchKernelGGL((gemm_pp_kernel<DT, TCU_RING>), dim3(grid), dim3(512), 0, stream,
                        (const unsigned char *)a.A, (const unsigned char *)a.B,
                        (unsigned char *)a.C, (int)a.K, a.lda, a.ldb, a.ldc, a.accum ? 1 : 0,
-                       tm, tn, nsplit);
+                       tm, tn, nsplit, TileRemap{});
     return hipGetLastError();
   }
   // Element-wise operand access (pitches not multiples of 16 bytes).
@@ -672,38 +710,63 @@ hipError_t launch_dt(const RectArgs &a, hipStream_t stream, int num_cus) {
 
 }  // namespace
 
+// The transitive closure's matrix-core phases for the pivot band
+// [k0, k0 + Bk), Y = X[band, band] already closed.  Every phase is the D
+// formula X[I, J] |= X[I, band] X[band, J] over a set of tiles, computed in
+// place.  Tiles may read operand blocks that other tiles of the same launch
+// are rewriting; that is harmless because every value only grows (0 -> 1)
+// and stays between its value before the phase and the closure: with one
+// operand final (Y, or a panel finished by an earlier launch), any mix of
+// old and new values in the other gives exactly the final product.
+//   * column panel: X[I, band] |= X[I, band] Y for I outside the band;
+//   * then, in one launch, the row panel X[band, J] |= Y X[band, J] and the
+//     rest X[I, J] |= X[I, band] X[band, J]: all tiles with J outside the
+//     band (the column panel is final, so the rows I = band and I outside
+//     it take the same formula).
 hipError_t launch_tc_panels(unsigned char *X, int64_t ld, int n, int k0, int Bk,
                             hipStream_t stream) {
-  // Pivot row band X[k0:k0+Bk, J] |= Y X[k0:k0+Bk, J] and pivot column band
-  // X[I, k0:k0+Bk] |= X[I, k0:k0+Bk] Y for J, I outside the band, Y the closed
-  // diagonal block.  Each tile spans the whole band (256 rows, resp.
-  // columns), so it reads exactly the band elements it rewrites and no other
-  // tile touches them.
-  unsigned char *band_row = X + (int64_t)k0 * ld;
   unsigned char *band_col = X + k0;
   const unsigned char *Y = X + (int64_t)k0 * ld + k0;
-  const bool vec = ld % 16 == 0;
-  hipError_t e;
-  if (vec) {
-    e = launch_bool<256, 64, true>(Y, band_row, band_row, ld, Bk, n, Bk, k0, false, true, stream);
-    if (e != hipSuccess) return e;
+  if (ld % 16 == 0)
     return launch_bool<64, 256, true>(band_col, Y, band_col, ld, n, Bk, Bk, k0, true, false,
                                       stream);
-  }
-  e = launch_bool<256, 64, false>(Y, band_row, band_row, ld, Bk, n, Bk, k0, false, true, stream);
-  if (e != hipSuccess) return e;
   return launch_bool<64, 256, false>(band_col, Y, band_col, ld, n, Bk, Bk, k0, true, false,
                                      stream);
 }
 
 hipError_t launch_tc_rest(unsigned char *X, int64_t ld, int n, int k0, int Bk,
-                          hipStream_t stream) {
-  // X[I, J] |= X[I, k0:k0+Bk] X[k0:k0+Bk, J] for I, J outside the band: the
-  // D function, with x and + on the matrix cores and min(., 1) on the way out.
+                          hipStream_t stream, int num_cus) {
   const unsigned char *L = X + k0;
   const unsigned char *R = X + (int64_t)k0 * ld;
-  if (ld % 16 == 0) return launch_bool<128, 128, true>(L, R, X, ld, n, n, Bk, k0, true, true, stream);
-  return launch_bool<128, 128, false>(L, R, X, ld, n, n, Bk, k0, true, true, stream);
+  // Whole 256-wide bands and 16-byte rows: the full-tile kernel over
+  // n/256 x (n/256 - 1) tiles, stepping over the band's tile column.
+  if (tc_full_tiles(n, Bk, ld)) {
+    TileRemap rm;
+    rm.band_n = k0 / 256;
+    rm.skip_n = 256;
+    return launch_tc_tiles(X, ld, k0, n / 256, n / 256 - 1, rm, stream, num_cus);
+  }
+  if (ld % 16 == 0)
+    return launch_bool<128, 128, true>(L, R, X, ld, n, n, Bk, k0, false, true, stream);
+  return launch_bool<128, 128, false>(L, R, X, ld, n, n, Bk, k0, false, true, stream);
+}
+
+bool tc_full_tiles(int64_t n, int Bk, int64_t ld) {
+  return n % 256 == 0 && Bk == 256 && ld % 16 == 0 && 256 * ld < ((int64_t)1 << 32);
+}
+
+hipError_t launch_tc_tiles(unsigned char *X, int64_t ld, int k0, int tiles_m, int tiles_n,
+                           const TileRemap &remap, hipStream_t stream, int num_cus) {
+  // The D formula X[I, J] |= X[I, band] X[band, J] (band = [k0, k0 + 256))
+  // on a tiles_m x tiles_n grid of 256 x 256 tiles placed by remap, by at
+  // most num_cus persistent workgroups.
+  const int items = tiles_m * tiles_n;
+  if (items <= 0) return hipSuccess;
+  const int grid = num_cus < items ? num_cus : items;
+  hipLaunchKernelGGL((gemm_pp_kernel<TCU_I8_BOOL, TCU_RING>), dim3(grid), dim3(512), 0, stream,
+                     X + k0, X + (int64_t)k0 * ld, X, 256, ld, ld, ld, 1, tiles_m, tiles_n, 1,
+                     remap);
+  return hipGetLastError();
 }
 
 hipError_t launch_rect(int dtype, int s, const RectArgs &a, hipStream_t stream, int num_cus) {

@@ -7,6 +7,17 @@
 
 namespace tcu {
 
+constexpr int kNoBand = 0x7fffffff;
+
+// Placement of a full-tile kernel's tile grid in the output: tile row tm
+// starts at m_base + 256 tm, plus skip_m once tm >= band_m (the same for
+// columns).  The identity by default; the transitive closure uses it to
+// step over the pivot bands another launch owns.
+struct TileRemap {
+  int m_base = 0, band_m = kNoBand, skip_m = 0;
+  int n_base = 0, band_n = kNoBand, skip_n = 0;
+};
+
 // Native call: C (n x s) = A (n x s) * B (s x s) [+ C when accum], for s in
 // {16, 32}, contiguous operands.
 hipError_t launch_tall(int dtype, int s, const void *A, int64_t n, const void *B, void *C,
@@ -30,12 +41,18 @@ hipError_t launch_rect(int dtype, int s, const RectArgs &args, hipStream_t strea
 // Transitive closure, in place on an n x n int8 0/1 matrix X with row pitch
 // ld: all pivot bands of Bk <= 256 vertices in order (see tcu_tc.hip).
 hipError_t launch_tc(unsigned char *X, int64_t ld, int64_t n, hipStream_t stream, int num_cus);
-// Its matrix-core phases for the band [k0, k0 + Bk): the pivot row and column
-// bands, then the rest of the matrix (tcu_gemm.hip).
+// Its matrix-core phases for the band [k0, k0 + Bk): the pivot column band,
+// then the pivot row band together with the rest of the matrix
+// (tcu_gemm.hip).
 hipError_t launch_tc_panels(unsigned char *X, int64_t ld, int n, int k0, int Bk,
                             hipStream_t stream);
 hipError_t launch_tc_rest(unsigned char *X, int64_t ld, int n, int k0, int Bk,
-                          hipStream_t stream);
+                          hipStream_t stream, int num_cus);
+// Whether the full-tile kernel takes the D updates (n a multiple of 256,
+// whole bands, 16-byte row pitch), and its launch on a remapped tile grid.
+bool tc_full_tiles(int64_t n, int Bk, int64_t ld);
+hipError_t launch_tc_tiles(unsigned char *X, int64_t ld, int k0, int tiles_m, int tiles_n,
+                           const TileRemap &remap, hipStream_t stream, int num_cus);
 
 // Batch polynomial evaluation: out[i] = sum_{h<n} coef[h] * pts[i]^h for
 // i < np, 16-bit inputs (dtype TCU_F16_F32, TCU_BF16_F32 or TCU_BF16_BF16).

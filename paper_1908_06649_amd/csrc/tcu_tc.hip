@@ -17,10 +17,13 @@
 // reads and writes all n^2 bytes) by 8.
 //   * normalize: every nonzero byte becomes 1 (nonzero = edge);
 //   * per band [k0, k0 + Bk):
-//       diag  -- one workgroup: the block as 256-bit rows in LDS, then the
-//                iterative algorithm over k in the block: every row i with
-//                bit k set ORs row k into itself, one barrier per k;
-//       panels, rest -- gemm_kernel with the 0/1 output (tcu_gemm.hip).
+//       diag  -- one workgroup: the block as 256-bit rows in registers, the
+//                iterative algorithm over the block's pivots by sub-bands
+//                of 32 (see tc_diag_kernel);
+//       panels, rest -- the product kernels with the 0/1 output: the
+//                pivot column band, then the pivot row band and the rest
+//                in one launch (tcu_gemm.hip explains why the in-place
+//                updates may overlap).
 #include "tcu_device.h"
 #include "tcu_launch.h"
 
@@ -28,7 +31,6 @@ namespace tcu {
 namespace {
 
 constexpr int kBand = 256;           // pivot band width (vertices)
-constexpr int kDiagThreads = 1024;   // 16 waves; 2 row words each
 constexpr int kWordsPerRow = kBand / 32;
 
 // Every nonzero byte of the n x n matrix becomes 1.  Rows are walked by
@@ -55,70 +57,160 @@ __global__ __launch_bounds__(256) void tc_normalize_kernel(unsigned char *__rest
   }
 }
 
-// Close the Bk x Bk diagonal block at D (row pitch ld), Bk <= 256.
-__global__ __launch_bounds__(kDiagThreads) void tc_diag_kernel(unsigned char *__restrict__ D,
-                                                               int64_t ld, int Bk) {
-  __shared__ unsigned bits[kBand][kWordsPerRow];
+// 4 bytes holding 0/1 -> 4 bits, and back.
+__device__ __forceinline__ unsigned bytes_to_bits4(unsigned x) {
+  return (x & 1u) | ((x >> 7) & 2u) | ((x >> 14) & 4u) | ((x >> 21) & 8u);
+}
+__device__ __forceinline__ unsigned bits4_to_bytes(unsigned b) {
+  return (b & 1u) | ((b & 2u) << 7) | ((b & 4u) << 14) | ((b & 8u) << 21);
+}
+
+// Value of lane h (0..3) of each group of 4 consecutive lanes (DPP quad
+// permutation; h wave-uniform).
+__device__ __forceinline__ unsigned quad_broadcast(unsigned v, int h) {
+  switch (h) {
+    case 0: return (unsigned)__builtin_amdgcn_update_dpp(0, (int)v, 0x00, 0xf, 0xf, false);
+    case 1: return (unsigned)__builtin_amdgcn_update_dpp(0, (int)v, 0x55, 0xf, 0xf, false);
+    case 2: return (unsigned)__builtin_amdgcn_update_dpp(0, (int)v, 0xaa, 0xf, 0xf, false);
+    default: return (unsigned)__builtin_amdgcn_update_dpp(0, (int)v, 0xff, 0xf, 0xf, false);
+  }
+}
+
+// Close the Bk x Bk diagonal block at D (row pitch ld; entries already 0/1),
+// Bk <= 256.  Row i is held as 8 words of bits by the 4 threads 4i .. 4i+3
+// (two words each).  The pivots are taken in sub-bands K of 32; for each:
+//   * the pivots' current rows are published to LDS;
+//   * one wave closes the 32 x 32 block of K's rows and columns (the
+//     iterative algorithm on 32 one-word rows, the pivot row broadcast with
+//     readlane), giving T*[k]: the pivots reachable from pivot k through K,
+//     k included;
+//   * every row i (pivot or not) forms R_i, the union of T*[k] over the
+//     pivots k it has an edge to, and ORs in the published rows of R_i.
+// That is the iterative algorithm's 32 steps over K: a vertex reaches v
+// through K exactly when some pivot it reaches through K has an edge to v.
+template <bool kVec>
+__global__ __launch_bounds__(1024) void tc_diag_kernel(unsigned char *__restrict__ D, int64_t ld,
+                                                       int Bk) {
+  __shared__ __attribute__((aligned(16))) unsigned krow[32][kWordsPerRow];
+  __shared__ unsigned tstar[32];
   const int t = threadIdx.x;
-  const int i = t >> 2;                  // row
-  const int w0 = 2 * (t & 3);            // this thread's two words of row i
+  const int i = t >> 2;              // row
+  const int w0 = 2 * (t & 3);        // this thread's words w0, w0 + 1 of row i
+  unsigned row[2];
   // bytes -> bits (bit b of word w = column 32w + b)
+  const unsigned char *src = D + (int64_t)i * ld;
 #pragma unroll
   for (int q = 0; q < 2; ++q) {
     const int w = w0 + q;
     unsigned word = 0;
     if (i < Bk) {
-      const unsigned char *row = D + (int64_t)i * ld + 32 * w;
-      for (int b = 0; b < 32; ++b)
-        if (32 * w + b < Bk && row[b] != 0) word |= 1u << b;
+      if (kVec && 32 * w + 32 <= Bk) {
+        const u32x4 a = *(const u32x4 *)(src + 32 * w);
+        const u32x4 b = *(const u32x4 *)(src + 32 * w + 16);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          word |= bytes_to_bits4(a[c]) << (4 * c);
+          word |= bytes_to_bits4(b[c]) << (16 + 4 * c);
+        }
+      } else {
+        for (int b = 0; b < 32; ++b)
+          if (32 * w + b < Bk && src[32 * w + b]) word |= 1u << b;
+      }
     }
-    bits[i][w] = word;
+    row[q] = word;
   }
-  __syncthreads();
-  // The iterative algorithm on the block, k in order.  Bit k of row i is
-  // stable during step k (row k only ORs itself into itself), so one
-  // barrier per step orders every read and write.
-  for (int k = 0; k < Bk; ++k) {
-    if ((bits[i][k >> 5] >> (k & 31)) & 1u) {
-      bits[i][w0] |= bits[k][w0];
-      bits[i][w0 + 1] |= bits[k][w0 + 1];
+#pragma unroll
+  for (int sb = 0; sb < kWordsPerRow; ++sb) {
+    if (32 * sb >= Bk) break;
+    const int nk = Bk - 32 * sb < 32 ? Bk - 32 * sb : 32;   // pivots in this sub-band
+    const unsigned kmask = nk == 32 ? ~0u : (1u << nk) - 1u;
+    if (i >= 32 * sb && i < 32 * sb + 32) {
+      krow[i - 32 * sb][w0] = row[0];
+      krow[i - 32 * sb][w0 + 1] = row[1];
     }
     __syncthreads();
+    // (Pivots past nk have zero rows and no bits in kmask, so the loops
+    // below run all 32 steps, fully unrolled, with no effect from them.)
+    if (t < 32) {
+      unsigned tk = krow[t][sb] & kmask;
+#pragma unroll
+      for (int kk = 0; kk < 32; ++kk) {
+        const unsigned pivot = (unsigned)__builtin_amdgcn_readlane((int)tk, kk);
+        tk |= pivot & (0u - ((tk >> kk) & 1u));
+      }
+      tstar[t] = tk | (1u << t);
+    }
+    __syncthreads();
+    // word sb of row i, from the quad lane that holds it
+    const unsigned wsb = quad_broadcast((sb & 1) ? row[1] : row[0], sb >> 1);
+    const unsigned edges = wsb & kmask;
+    unsigned reach = 0;
+#pragma unroll
+    for (int kk = 0; kk < 32; ++kk) reach |= tstar[kk] & (0u - ((edges >> kk) & 1u));
+    reach &= kmask;
+#pragma unroll
+    for (int kk = 0; kk < 32; ++kk) {
+      const unsigned m = 0u - ((reach >> kk) & 1u);
+      row[0] |= krow[kk][w0] & m;
+      row[1] |= krow[kk][w0 + 1] & m;
+    }
+    __syncthreads();   // krow and tstar are rewritten by the next sub-band
   }
   // bits -> bytes
   if (i < Bk) {
+    unsigned char *dst = D + (int64_t)i * ld;
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
       const int w = w0 + q;
-      const unsigned word = bits[i][w];
-      unsigned char *row = D + (int64_t)i * ld + 32 * w;
-      for (int b = 0; b < 32; ++b)
-        if (32 * w + b < Bk) row[b] = (unsigned char)((word >> b) & 1u);
+      if (kVec && 32 * w + 32 <= Bk) {
+        u32x4 a, b;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          a[c] = bits4_to_bytes(row[q] >> (4 * c));
+          b[c] = bits4_to_bytes(row[q] >> (16 + 4 * c));
+        }
+        *(u32x4 *)(dst + 32 * w) = a;
+        *(u32x4 *)(dst + 32 * w + 16) = b;
+      } else {
+        for (int b = 0; b < 32; ++b)
+          if (32 * w + b < Bk) dst[32 * w + b] = (unsigned char)((row[q] >> b) & 1u);
+      }
     }
   }
 }
+
+hipError_t launch_diag(unsigned char *X, int64_t ld, int64_t k0, int Bk, bool vec,
+                       hipStream_t stream) {
+  if (vec)
+    hipLaunchKernelGGL(tc_diag_kernel<true>, dim3(1), dim3(1024), 0, stream, X + k0 * ld + k0, ld,
+                       Bk);
+  else
+    hipLaunchKernelGGL(tc_diag_kernel<false>, dim3(1), dim3(1024), 0, stream, X + k0 * ld + k0,
+                       ld, Bk);
+  return hipGetLastError();
+}
+
+#define TCU_TRY(x)                   \
+  do {                               \
+    const hipError_t e_ = (x);       \
+    if (e_ != hipSuccess) return e_; \
+  } while (0)
 
 }  // namespace
 
 hipError_t launch_tc(unsigned char *X, int64_t ld, int64_t n, hipStream_t stream, int num_cus) {
   if (n <= 0) return hipSuccess;
   const int64_t rows_grid = n < (int64_t)num_cus * 8 ? n : (int64_t)num_cus * 8;
-  const int vec = (ld % 16 == 0 && (reinterpret_cast<uintptr_t>(X) & 15) == 0) ? 1 : 0;
+  const bool vec = ld % 16 == 0 && (reinterpret_cast<uintptr_t>(X) & 15) == 0;
   hipLaunchKernelGGL(tc_normalize_kernel, dim3((unsigned)rows_grid), dim3(256), 0, stream, X, n,
-                     ld, vec);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+                     ld, vec ? 1 : 0);
+  TCU_TRY(hipGetLastError());
   for (int64_t k0 = 0; k0 < n; k0 += kBand) {
     const int Bk = (int)(n - k0 < kBand ? n - k0 : kBand);
-    hipLaunchKernelGGL(tc_diag_kernel, dim3(1), dim3(kDiagThreads), 0, stream,
-                       X + k0 * ld + k0, ld, Bk);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
+    TCU_TRY(launch_diag(X, ld, k0, Bk, vec, stream));
     if (n == Bk) break;
-    e = launch_tc_panels(X, ld, (int)n, (int)k0, Bk, stream);
-    if (e != hipSuccess) return e;
-    e = launch_tc_rest(X, ld, (int)n, (int)k0, Bk, stream);
-    if (e != hipSuccess) return e;
+    TCU_TRY(launch_tc_panels(X, ld, (int)n, (int)k0, Bk, stream));
+    TCU_TRY(launch_tc_rest(X, ld, (int)n, (int)k0, Bk, stream, num_cus));
   }
   return hipSuccess;
 }

@@ -40,7 +40,8 @@ def graph(n, deg, seed):
     return inputs.digraph(n, deg, seed).numpy().view(np.uint8)
 
 
-SIZES = [1, 2, 15, 16, 17, 100, 255, 256, 257, 300, 511, 512, 513, 600, 1000, 1024, 1500]
+SIZES = [1, 2, 15, 16, 17, 100, 255, 256, 257, 300, 511, 512, 513, 600, 768, 1000, 1024, 1280,
+         1500, 2048]
 
 
 @pytest.mark.parametrize("deg", [0.7, 1.3, 3.0])
@@ -56,7 +57,7 @@ def test_tc_pitched(n, ld):
     assert np.array_equal(run_tc(d, ld), oracle.transitive_closure(d))
 
 
-@pytest.mark.parametrize("n", [700, 2000])
+@pytest.mark.parametrize("n", [700, 1536, 2000, 2560])
 def test_tc_long_paths_cross_every_band(n):
     """A path i -> i+1 (closure: strict upper triangle) and its reverse:
     reachability has to travel through every pivot band."""
@@ -68,6 +69,20 @@ def test_tc_long_paths_cross_every_band(n):
     p = np.zeros((n, n), np.uint8)
     p[perm[:-1], perm[1:]] = 1
     assert np.array_equal(run_tc(p), oracle.transitive_closure(p))
+
+
+@pytest.mark.parametrize("n", [512, 1024, 1792])
+def test_tc_structured_across_bands(n):
+    """Graphs whose reachability must cross band boundaries in both
+    directions (whole bands: the look-ahead schedule): a few long cycles
+    woven through every band, plus a sparse random layer."""
+    rng = np.random.default_rng(n)
+    d = np.zeros((n, n), np.uint8)
+    for _ in range(3):
+        perm = rng.permutation(n)[: n // 3]
+        d[perm, np.roll(perm, 1)] = 1
+    d |= graph(n, 0.3, n + 1)
+    assert np.array_equal(run_tc(d), oracle.transitive_closure(d))
 
 
 def test_tc_cycle_and_empty():
