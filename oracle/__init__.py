@@ -19,6 +19,11 @@ numpy in/out:
 * ``transitive_closure(d)`` -- reachability by paths of >= 1 edge from an
   n x n 0/1 adjacency matrix (Section 4.3), by the in-place iterative
   algorithm the section starts from (k outermost, then i, then j).
+* ``dft_direct(x)`` -- the DFT by its definition y = x^T W, W[r][c] =
+  exp(-2 pi i r c / n) (Section 4.5), O(n^2) per vector, binary64;
+  ``dft(x)`` -- the same transform through numpy's binary64 FFT (a library
+  routine standing in for the definition at sizes where O(n^2) is too slow;
+  pinned against ``dft_direct``).
 * ``mm_acc(A, B, C0, dtype, out)`` -- the accumulating form ``C0 + A*B``
   that the D functions of Sections 4.2 and 4.3 ask of the unit
   (X <- X + Y*Z); C0 holds stored output values ('f32', 'bf16' bits or
@@ -67,6 +72,8 @@ def _load():
     lib.oracle_poly_eval.restype = ctypes.c_int
     lib.oracle_transitive_closure.argtypes = [vp, i64, vp]
     lib.oracle_transitive_closure.restype = ctypes.c_int
+    lib.oracle_dft_direct.argtypes = [vp, i64, i64, vp]
+    lib.oracle_dft_direct.restype = ctypes.c_int
     lib.oracle_threads.argtypes = []
     lib.oracle_threads.restype = ctypes.c_int
     _lib = lib
@@ -186,3 +193,22 @@ def transitive_closure(d: np.ndarray) -> np.ndarray:
     if rc != 0:
         raise ValueError("oracle rejected its arguments")
     return out
+
+
+def dft_direct(x: np.ndarray) -> np.ndarray:
+    """DFT of every row of x (complex, shape (batch, n) or (n,)) by the
+    definition, in binary64; returns complex128 of the same shape."""
+    x = np.asarray(x, dtype=np.complex128)
+    shape = x.shape
+    x2 = np.ascontiguousarray(x.reshape(-1, shape[-1]))
+    y = np.empty_like(x2)
+    rc = _load().oracle_dft_direct(_ptr(x2.view(np.float64)), x2.shape[1], x2.shape[0],
+                                   _ptr(y.view(np.float64)))
+    if rc != 0:
+        raise ValueError("oracle rejected its arguments")
+    return y.reshape(shape)
+
+
+def dft(x: np.ndarray) -> np.ndarray:
+    """DFT of every row of x (complex) in binary64 through numpy's FFT."""
+    return np.fft.fft(np.asarray(x, dtype=np.complex128), axis=-1)

@@ -308,3 +308,35 @@ int oracle_transitive_closure(const uint8_t *d, int64_t n, uint8_t *out)
     free(bits);
     return 0;
 }
+
+/* ----------------------------------------------- discrete Fourier transform */
+/*
+ * Section 4.5 defines the DFT of an n-vector x as y = x^T W with the Fourier
+ * matrix W[r][c] = exp(-2 pi i r c / n).  This is that definition, one
+ * output at a time: y[k] = sum_j x[j] (cos t - i sin t), t = 2 pi (j k mod n)
+ * / n, in binary64 (the product j k is reduced mod n exactly in integers
+ * first).  x, y: batch * n complex values as interleaved (re, im) doubles.
+ * O(n^2) per vector: for checking small sizes and for pinning.
+ */
+int oracle_dft_direct(const double *x, int64_t n, int64_t batch, double *y)
+{
+    if (n < 1 || batch < 0) return -1;
+    const double two_pi = 6.283185307179586476925286766559;
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int64_t b = 0; b < batch; ++b)
+        for (int64_t k = 0; k < n; ++k) {
+            const double *xb = x + 2 * b * n;
+            double re = 0.0, im = 0.0;
+            for (int64_t j = 0; j < n; ++j) {
+                const int64_t e = (int64_t)(((unsigned __int128)j * (unsigned __int128)k) % (unsigned __int128)n);
+                const double t = two_pi * (double)e / (double)n;
+                const double c = cos(t), s = sin(t);
+                /* (xr + i xi)(c - i s) */
+                re += xb[2 * j] * c + xb[2 * j + 1] * s;
+                im += xb[2 * j + 1] * c - xb[2 * j] * s;
+            }
+            y[2 * (b * n + k)] = re;
+            y[2 * (b * n + k) + 1] = im;
+        }
+    return 0;
+}

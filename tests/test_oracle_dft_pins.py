@@ -1,0 +1,103 @@
+"""Pins of the oracle's DFT (Section 4.5) against what the mathematics fixes
+(CPU only).
+
+dft_direct is the definition y[k] = sum_j x[j] exp(-2 pi i j k / n).  It is
+checked against closed-form transforms (a unit impulse, a constant, a pure
+complex exponential, a cosine, a shifted impulse), Parseval's identity,
+linearity, the circular shift theorem and the transform of the conjugate,
+and against exact rational arithmetic on sizes where the twiddles are exact
+(n = 1, 2, 4: W entries in {+-1, +-i}).  numpy's FFT (oracle.dft, used at
+large sizes) is checked against dft_direct.  Plausible mistakes (the
+conjugate sign, the transpose of a non-symmetric use, an off-by-one
+frequency) fail the pins.
+"""
+import numpy as np
+import pytest
+
+import oracle
+
+RNG = np.random.default_rng(42)
+
+
+def rand_c(shape):
+    return RNG.standard_normal(shape) + 1j * RNG.standard_normal(shape)
+
+
+@pytest.mark.parametrize("n", [1, 2, 3, 8, 17, 64, 100])
+def test_dft_closed_forms(n):
+    delta = np.zeros(n, complex)
+    delta[0] = 1
+    assert np.allclose(oracle.dft_direct(delta), np.ones(n), atol=1e-14)
+    assert np.allclose(oracle.dft_direct(np.ones(n, complex)),
+                       np.eye(1, n, 0).ravel() * n, atol=1e-10)
+    for f in range(min(n, 5)):
+        e = np.exp(2j * np.pi * f * np.arange(n) / n)        # exp(+2 pi i f j / n)
+        want = np.zeros(n, complex)
+        want[f] = n
+        assert np.allclose(oracle.dft_direct(e), want, atol=1e-9 * n)
+    if n > 2:
+        c = np.cos(2 * np.pi * 1 * np.arange(n) / n)
+        want = np.zeros(n, complex)
+        want[1] += n / 2
+        want[n - 1] += n / 2
+        assert np.allclose(oracle.dft_direct(c), want, atol=1e-9 * n)
+        shifted = np.zeros(n, complex)
+        shifted[2] = 1                                          # x = delta[j - 2]
+        assert np.allclose(oracle.dft_direct(shifted),
+                           np.exp(-2j * np.pi * 2 * np.arange(n) / n), atol=1e-12)
+
+
+@pytest.mark.parametrize("n", [1, 2, 4])
+def test_dft_exact_small(n):
+    """For n <= 4 every entry of W is +-1 or +-i: against that matrix, written
+    out by hand, on small integers (the definition's binary64 cos/sin of
+    pi and pi/2 are off by at most 2^-53 of a unit)."""
+    x = RNG.integers(-5, 6, (6, n)) + 1j * RNG.integers(-5, 6, (6, n))
+    w = np.array([[1, 1, 1, 1], [1, -1j, -1, 1j], [1, -1, 1, -1], [1, 1j, -1, -1j]])[:n, :n]
+    if n == 2:
+        w = np.array([[1, 1], [1, -1]])
+    want = x @ w
+    mag = np.sum(np.abs(x), axis=1, keepdims=True)
+    assert np.all(np.abs(oracle.dft_direct(x) - want) <= 4 * 2.0 ** -52 * mag)
+
+
+def test_dft_identities():
+    n = 96
+    x, z = rand_c((4, n)), rand_c((4, n))
+    X, Z = oracle.dft_direct(x), oracle.dft_direct(z)
+    assert np.allclose(np.sum(np.abs(X) ** 2, axis=1), n * np.sum(np.abs(x) ** 2, axis=1))
+    assert np.allclose(oracle.dft_direct(2.5 * x - 1j * z), 2.5 * X - 1j * Z)
+    m = 7
+    xs = np.roll(x, m, axis=1)                                   # x[j - m]
+    assert np.allclose(oracle.dft_direct(xs), X * np.exp(-2j * np.pi * m * np.arange(n) / n))
+    # DFT(conj(x))[k] = conj(DFT(x)[-k])
+    assert np.allclose(oracle.dft_direct(np.conj(x)), np.conj(np.roll(X[:, ::-1], 1, axis=1)))
+
+
+@pytest.mark.parametrize("n", [2, 32, 256, 2048])
+def test_fft_matches_definition(n):
+    x = rand_c((3, n))
+    d, f = oracle.dft_direct(x), oracle.dft(x)
+    assert np.max(np.abs(d - f)) <= 1e-9 * np.sum(np.abs(x), axis=1).max()
+
+
+def _mutants():
+    def conj_sign(x):
+        return np.conj(oracle.dft_direct(np.conj(x)))           # exp(+2 pi i jk/n)
+
+    def off_by_one(x):
+        return np.roll(oracle.dft_direct(x), 1, axis=-1)
+
+    def unnormalized_half(x):
+        return oracle.dft_direct(x) / 2
+
+    return [conj_sign, off_by_one, unnormalized_half]
+
+
+def test_pins_catch_planted_mistakes():
+    n = 8
+    shifted = np.zeros(n, complex)
+    shifted[2] = 1
+    want = np.exp(-2j * np.pi * 2 * np.arange(n) / n)
+    for mut in _mutants():
+        assert not np.allclose(mut(shifted), want, atol=1e-12), mut.__name__
