@@ -19,6 +19,9 @@ JSON line:
   poly       batch polynomial evaluation (tcu_poly_eval, Theorem 11) on 2^24
              points with 4096 coefficients: TFLOP/s of the method's 2pn
              multiply-adds vs the bf16 matrix-core peak
+  dft        DFT (tcu_dft, Theorem 7) of 16 complex64 vectors of 2^20: GB/s of
+             the levels' traffic (each of the ceil(log_32 n) levels reads and
+             writes the array once) vs HBM peak, and 5 n log2 n GFLOP/s
   tc         transitive closure (tcu_transitive_closure, Theorem 5) of a
              random 8192-vertex digraph: GB/s of the D updates' algorithmic
              traffic (each pivot band reads and writes the off-band n^2 bytes)
@@ -43,6 +46,7 @@ from __future__ import annotations
 import argparse
 import hashlib
 import json
+import math
 import os
 import re
 import sys
@@ -64,7 +68,7 @@ PROFILES = os.path.join(ROOT, "profiles")
 
 def kernel_sources(kind: str):
     main = {"gemm": ["tcu_gemm.hip"], "rect": ["tcu_gemm.hip"], "poly": ["tcu_poly.hip"],
-            "tc": ["tcu_tc.hip", "tcu_gemm.hip"]}.get(kind, ["tcu_tall.hip"])
+            "tc": ["tcu_tc.hip", "tcu_gemm.hip"], "dft": ["tcu_dft.hip"]}.get(kind, ["tcu_tall.hip"])
     return [os.path.join(CSRC, f) for f in (*main, "tcu_device.h")]
 
 
@@ -105,6 +109,13 @@ def algorithmic(spec: dict):
         n, s = spec["n"], spec["s"]
         return 2.0 * n * s * s, n * s * ib + s * s * ib + n * s * ob
     del inputs
+    if spec["kind"] == "dft":
+        n, b, s = spec["n"], spec["batch"], spec["s"]
+        levels, m = 1, s
+        while m < n:
+            m *= s
+            levels += 1
+        return 5.0 * b * n * math.log2(n), levels * 2 * 8 * b * n
     if spec["kind"] == "tc":
         # per pivot band of up to 256 vertices: the D update reads and writes
         # every off-band entry once, the panel updates their band entries
@@ -133,9 +144,17 @@ class Workload:
         from paper_1908_06649_amd import inputs, tcu
         self.name = name
         self.spec = (inputs.WORKLOADS.get(name) or inputs.RECT_WORKLOADS.get(name)
-                     or inputs.POLY_WORKLOADS.get(name) or inputs.TC_WORKLOADS[name])
+                     or inputs.POLY_WORKLOADS.get(name) or inputs.TC_WORKLOADS.get(name)
+                     or inputs.DFT_WORKLOADS[name])
         self.tcu = tcu
         self.s = self.spec["s"]
+        if self.spec["kind"] == "dft":
+            sp = self.spec
+            self.A = inputs.complex_signal(sp["batch"], sp["n"], sp["seed"])
+            self.dA = self.A.cuda()
+            self.C = torch.empty_like(self.dA)
+            self.W = torch.empty_like(self.dA)
+            return
         if self.spec["kind"] == "tc":
             # the closure is computed in place; the algorithm's work does not
             # depend on the data, so repeated calls on the same array time it
@@ -162,6 +181,8 @@ class Workload:
         sp = self.spec
         if sp["kind"] == "gemm":
             self.tcu.tcu_gemm(self.dA, self.dB, self.C, sp["N"])
+        elif sp["kind"] == "dft":
+            self.tcu.tcu_dft(self.dA, self.C, self.W, sp["n"], sp["batch"])
         elif sp["kind"] == "tc":
             self.tcu.tcu_transitive_closure(self.dA, sp["n"], sp["n"])
         elif sp["kind"] == "poly":
@@ -224,7 +245,15 @@ def measure(name: str, steps: int, warmup: int) -> dict:
     kind = sp["kind"]
     out = {"workload": name, "ms_per_call": ms, "calls": calls, "square_calls": squares,
            "model_work": work}
-    if kind == "tc":
+    if kind == "dft":
+        gbs = nbytes / (ms * 1e-3) / 1e9
+        out.update({"value": gbs, "unit": "GB/s",
+                    "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS,
+                                 "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS,
+                                 "traffic": counted_traffic(name, kind)},
+                    "gflops_5nlogn": flops / (ms * 1e-3) / 1e9,
+                    "algorithmic_bytes": nbytes})
+    elif kind == "tc":
         gbs = nbytes / (ms * 1e-3) / 1e9
         out.update({"value": gbs, "unit": "GB/s",
                     "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS,
@@ -346,6 +375,7 @@ def main() -> int:
     ap.add_argument("--no-rect", action="store_true")
     ap.add_argument("--no-poly", action="store_true")
     ap.add_argument("--no-tc", action="store_true")
+    ap.add_argument("--no-dft", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--copy-probe", action="store_true")
@@ -366,7 +396,7 @@ def main() -> int:
         copy_probe()
         return 0
     known = {**inputs.WORKLOADS, **inputs.RECT_WORKLOADS, **inputs.POLY_WORKLOADS,
-             **inputs.TC_WORKLOADS}
+             **inputs.TC_WORKLOADS, **inputs.DFT_WORKLOADS}
     if args.workload not in known:
         names = sorted(known)
         print(f"unknown workload {args.workload}; choose from {names}", file=sys.stderr)
@@ -386,14 +416,15 @@ def main() -> int:
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": sp.get("dtype", "u8"),
+        "dtype": sp.get("dtype", "c64" if sp["kind"] == "dft" else "u8"),
         "data": "synthetic (seeded i.i.d. matrices; the paper has no datasets)",
         "config": {"workload": args.workload,
                    **{k: sp[k] for k in ("kind", "M", "K", "N", "n", "p", "s", "acc", "deg")
                       if k in sp},
                    "dtype_in": sp.get("dtype", "u8"), "dtype_out": sp.get("out", "u8"),
-                   "distribution": sp.get("dist", "coefficients N(0,1), points U[-1,1)"
-                                          if sp["kind"] == "poly" else "random digraph"),
+                   "distribution": sp.get("dist", {"poly": "coefficients N(0,1), points U[-1,1)",
+                                                   "tc": "random digraph",
+                                                   "dft": "re, im ~ N(0,1)"}.get(sp["kind"])),
                    "seed": sp["seed"]},
         "roofline": main_res["roofline"],
     }
@@ -458,9 +489,22 @@ def main() -> int:
                                           "model_work")}
             torch.cuda.empty_cache()
         result["tc"] = tc
+    if not args.no_dft:
+        dft = {}
+        for name in inputs.DFT_WORKLOADS:
+            if name == args.workload:
+                continue
+            r = measure(name, args.steps, max(args.warmup, 5))
+            r.pop("_workload")
+            dft[name] = {k: r[k] for k in ("value", "unit", "ms_per_call", "roofline",
+                                           "gflops_5nlogn", "calls", "square_calls",
+                                           "model_work")}
+            torch.cuda.empty_cache()
+        result["dft"] = dft
     result["cost_model"] = cost
     result["kernel_source_sha256"] = {"gemm": kernel_hash("gemm"), "tall": kernel_hash("tall"),
-                                      "poly": kernel_hash("poly"), "tc": kernel_hash("tc")}
+                                      "poly": kernel_hash("poly"), "tc": kernel_hash("tc"),
+                                      "dft": kernel_hash("dft")}
     print(json.dumps(result), flush=True)
     return 0
 

@@ -16,6 +16,7 @@
  *   - tcu_gemm_rect: the same decomposition for rectangular, strided and
  *     accumulating products (Corollary 1; the D functions' update).
  *   - tcu_transitive_closure: the blocked transitive closure (Theorem 5).
+ *   - tcu_dft: the discrete Fourier transform by Cooley-Tukey (Theorem 7).
  *   - tcu_poly_eval: batch polynomial evaluation (Theorem 11).
  *
  * Throughout, s = sqrt(m) is the unit size (a machine parameter of the
@@ -246,6 +247,35 @@ int tcu_poly_eval_ex(const void *coef, int64_t n, const void *points, int64_t p,
  * with q = ceil(n/s), each of (q-1) square calls. */
 int tcu_transitive_closure(void *X, int64_t n, int64_t ld);
 int tcu_transitive_closure_ex(void *X, int64_t n, int64_t ld, int s, void *hip_stream);
+
+/* ---- discrete Fourier transform (Theorem 7, Section 4.5) ----
+ *
+ * y_b[k] = sum_{j<n} x_b[j] exp(-2 pi i j k / n), for b < batch: the DFT
+ * y = x^T W of each vector, W[r][c] = exp(-2 pi i r c / n).
+ * The section's Cooley-Tukey recursion with radix s = sqrt(m): per level,
+ * the DFTs of length s of n/s interleaved subsequences as the tall product
+ * X^T W_s (n/s rows through the unit), the twiddles w^(r c) and the
+ * transpose, for ceil(log_s n) levels (the last of radix n/s^(L-1) <= s).
+ * Complex products are real products on the unit; data and W enter as
+ * hi + lo bfloat16 words (about 2^-16 relative accuracy per level).
+ *   x: batch * n complex values, each two binary32 (re, im), vector b at
+ *      x + 2 b n floats; read only.
+ *   y: batch * n complex values, written; must not overlap x or work.
+ *   work: batch * n complex values of scratch the levels alternate through
+ *      (its contents are overwritten); must not overlap x or y; may be NULL
+ *      when n <= s (one level).
+ *   n: a power of two, 1 <= n <= TCU_MAX_DFT_N; batch >= 0 (0: no-op).
+ * The unit size and stream come from tcu_get_unit() / tcu_get_stream().
+ * Errors: TCU_ERR_NULL, TCU_ERR_SHAPE (n not a power of two or out of range,
+ * batch < 0, extent of 2^40 bytes or more), TCU_ERR_UNSUPPORTED,
+ * TCU_ERR_ALIGN (16-byte base alignment), TCU_ERR_OVERLAP,
+ * TCU_ERR_NO_DEVICE, TCU_ERR_HIP.
+ * Cost accounting: per vector and level, 4 calls (the complex product as
+ * four real ones) of n/R rows, R the level's radix. */
+#define TCU_MAX_DFT_N ((int64_t)1 << 30)
+int tcu_dft(const void *x, void *y, void *work, int64_t n, int64_t batch);
+int tcu_dft_ex(const void *x, void *y, void *work, int64_t n, int64_t batch, int s,
+               void *hip_stream);
 
 /* ---- cost accounting (Theorem 2 proof; Section 5 weak model) ----
  * tcu_calls:        logical tensor-unit calls issued (1 per tall call,

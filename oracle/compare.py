@@ -182,3 +182,28 @@ def check_poly(dtype_in: str, dtype_out: str, coef_bits, pt_bits, got, s: int,
     assert rep["violations"] == 0, rep
     assert rel <= rel_bar, rep
     return rep
+
+
+def check_dft(x: np.ndarray, got: np.ndarray, ref: np.ndarray | None = None) -> dict:
+    """Compare a GPU DFT (complex, rows = vectors) with the binary64 oracle:
+    relative Frobenius error <= 1e-3 per vector, and elementwise
+    |err_k| <= 1e-2 * sum_j |x_j| (the magnitude bound: |W| = 1).
+    ref: the oracle result when already computed."""
+    x = np.asarray(x, dtype=np.complex128).reshape(-1, np.asarray(x).shape[-1])
+    got = np.asarray(got, dtype=np.complex128).reshape(x.shape)
+    if ref is None:
+        from . import dft, dft_direct
+        ref = dft_direct(x) if x.shape[1] <= 1024 else dft(x)
+    ref = np.asarray(ref).reshape(x.shape)
+    err = np.abs(got - ref)
+    mag = np.sum(np.abs(x), axis=1, keepdims=True)
+    den = np.linalg.norm(ref, axis=1)
+    rel = np.where(den > 0, np.linalg.norm(got - ref, axis=1) / np.where(den > 0, den, 1), 0.0)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        ratio = np.where(mag > 0, err / mag, np.where(err > 0, np.inf, 0.0))
+    rep = {"max_rel_frob": float(rel.max(initial=0.0)),
+           "max_err_over_l1": float(ratio.max(initial=0.0))}
+    assert np.all(np.isfinite(got)), rep
+    assert rep["max_rel_frob"] <= REL_FROB, rep
+    assert rep["max_err_over_l1"] <= ELEM, rep
+    return rep

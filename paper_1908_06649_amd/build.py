@@ -14,7 +14,8 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libtcu.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
-SOURCES = ["tcu_abi.cpp", "tcu_tall.hip", "tcu_gemm.hip", "tcu_poly.hip", "tcu_tc.hip"]
+SOURCES = ["tcu_abi.cpp", "tcu_tall.hip", "tcu_gemm.hip", "tcu_poly.hip", "tcu_tc.hip",
+           "tcu_dft.hip"]
 ARCH = "gfx950"
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden",
@@ -26,7 +27,8 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden",
 # Per-source additions.  The polynomial kernel consumes every matrix-core
 # result with vector ALU work at once; the VGPR-destination form of the
 # instruction saves a register-file move per result value.
-EXTRA = {"tcu_poly.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+EXTRA = {"tcu_poly.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+         "tcu_dft.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 
 def hipcc() -> str:

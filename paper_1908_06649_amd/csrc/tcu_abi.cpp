@@ -188,6 +188,20 @@ int validate_tc(const void *X, int64_t n, int64_t ld, int s) {
   return TCU_OK;
 }
 
+int validate_dft(const void *x, const void *y, const void *work, int64_t n, int64_t batch, int s) {
+  if (!unit_ok(s)) return TCU_ERR_UNSUPPORTED;
+  if (n < 1 || n > TCU_MAX_DFT_N || (n & (n - 1)) != 0 || batch < 0) return TCU_ERR_SHAPE;
+  if (batch > 0 && n > ((int64_t)1 << 40) / 8 / batch) return TCU_ERR_SHAPE;
+  const int64_t bytes = batch * n * 8;
+  const bool need_work = tcu::dft_levels(n, s) > 1;
+  if (bytes > 0 && (!x || !y || (need_work && !work))) return TCU_ERR_NULL;
+  if (misaligned(x) || misaligned(y) || misaligned(work)) return TCU_ERR_ALIGN;
+  if (overlap(y, bytes, x, bytes)) return TCU_ERR_OVERLAP;
+  if (need_work && (overlap(work, bytes, x, bytes) || overlap(work, bytes, y, bytes)))
+    return TCU_ERR_OVERLAP;
+  return TCU_OK;
+}
+
 }  // namespace
 
 TCU_EXPORT int tcu_set_unit(int s) {
@@ -336,6 +350,37 @@ TCU_EXPORT int tcu_transitive_closure_ex(void *X, int64_t n, int64_t ld, int s,
 
 TCU_EXPORT int tcu_transitive_closure(void *X, int64_t n, int64_t ld) {
   return tcu_transitive_closure_ex(X, n, ld, g_cfg.s, g_cfg.stream);
+}
+
+TCU_EXPORT int tcu_dft_ex(const void *x, void *y, void *work, int64_t n, int64_t batch, int s,
+                          void *hip_stream) {
+  int rc = validate_dft(x, y, work, n, batch, s);
+  if (rc != TCU_OK) return rc;
+  if (batch == 0) return TCU_OK;
+  int num_cus = 0;
+  rc = device_ready(&num_cus);
+  if (rc != TCU_OK) return rc;
+  if (tcu::launch_dft(x, y, work, n, batch, s, (hipStream_t)hip_stream, num_cus) != hipSuccess)
+    return TCU_ERR_HIP;
+  // Theorem 7: per vector and level one tall call of n/R rows times W_R, a
+  // complex product counted as the section's four real products.
+  const int L = tcu::dft_levels(n, s);
+  int64_t P = 1, calls = 0, squares = 0;
+  for (int t = 1; t <= L; ++t) {
+    const int64_t R = t < L ? s : n / P;
+    const int64_t rows = n / R;
+    calls += 4 * batch;
+    squares += 4 * batch * ((rows + s - 1) / s);
+    P *= R;
+  }
+  g_calls.fetch_add(calls, std::memory_order_relaxed);
+  g_square_calls.fetch_add(squares, std::memory_order_relaxed);
+  g_work.fetch_add(squares * s * s, std::memory_order_relaxed);
+  return TCU_OK;
+}
+
+TCU_EXPORT int tcu_dft(const void *x, void *y, void *work, int64_t n, int64_t batch) {
+  return tcu_dft_ex(x, y, work, n, batch, g_cfg.s, g_cfg.stream);
 }
 
 TCU_EXPORT int64_t tcu_calls(void) { return g_calls.load(std::memory_order_relaxed); }

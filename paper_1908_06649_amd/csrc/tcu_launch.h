@@ -54,6 +54,13 @@ bool tc_full_tiles(int64_t n, int Bk, int64_t ld);
 hipError_t launch_tc_tiles(unsigned char *X, int64_t ld, int k0, int tiles_m, int tiles_n,
                            const TileRemap &remap, hipStream_t stream, int num_cus);
 
+// Forward DFT of `batch` complex64 vectors of length n (a power of two):
+// ceil(log_s n) Cooley-Tukey levels alternating between work and y, the last
+// writing y (see tcu_dft.hip).
+int dft_levels(int64_t n, int s);
+hipError_t launch_dft(const void *x, void *y, void *work, int64_t n, int64_t batch, int s,
+                      hipStream_t stream, int num_cus);
+
 // Batch polynomial evaluation: out[i] = sum_{h<n} coef[h] * pts[i]^h for
 // i < np, 16-bit inputs (dtype TCU_F16_F32, TCU_BF16_F32 or TCU_BF16_BF16).
 hipError_t launch_poly(int dtype, int s, const void *coef, int64_t n, const void *pts, int64_t np,

@@ -62,6 +62,12 @@ TC_WORKLOADS = {
     "tc_n8192_deg2": dict(kind="tc", n=8192, deg=2.0, s=32, seed=9),
 }
 
+# Workloads of the DFT (tcu_dft, Theorem 7): batch complex64 vectors of
+# length n, real and imaginary parts ~ N(0, 1).
+DFT_WORKLOADS = {
+    "dft_c64_n1048576_b16_s32": dict(kind="dft", n=1 << 20, batch=16, s=32, seed=10),
+}
+
 TORCH_DTYPE = {"f16": torch.float16, "bf16": torch.bfloat16, "i8": torch.int8,
                "f32": torch.float32, "i32": torch.int32}
 
@@ -127,6 +133,14 @@ def digraph(n: int, avg_out_degree: float, seed: int) -> torch.Tensor:
 def make_tc_input(spec: dict) -> torch.Tensor:
     """Adjacency matrix (int8 0/1) of a transitive-closure workload."""
     return digraph(spec["n"], spec["deg"], spec["seed"])
+
+
+def complex_signal(batch: int, n: int, seed: int) -> torch.Tensor:
+    """batch x n complex64 values, real and imaginary parts ~ N(0, 1), drawn
+    as one (batch, n, 2) float32 array."""
+    gen = torch.Generator(device="cpu")
+    gen.manual_seed(seed)
+    return torch.view_as_complex(torch.randn((batch, n, 2), generator=gen, dtype=torch.float32))
 
 
 def make_c0(spec: dict) -> torch.Tensor:

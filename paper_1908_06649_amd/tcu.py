@@ -8,6 +8,7 @@ fallback: if ``libtcu.so`` is missing or fails to load, every call raises.
     tcu_mm_tall(A, n, s, B, C)   C (n x s) = A (n x s) @ B (s x s)     (native call)
     tcu_gemm(A, B, C, N)         C (N x N) = A @ B, unit size tcu_get_unit()
     tcu_transitive_closure(X, n, ld)   X <- transitive closure, in place (Theorem 5)
+    tcu_dft(x, y, work, n, batch)   y[b] = DFT(x[b]), complex64        (Theorem 7)
     tcu_poly_eval(coef, n, points, p, out)
                                  out[i] = sum_h coef[h] * points[i]**h    (Theorem 11)
     tcu_gemm_rect(A, lda, B, ldb, C, ldc, M, K, N, flags)
@@ -63,6 +64,8 @@ SIGNATURES = {
     "tcu_poly_eval_ex": (_int, [_vp, _i64, _vp, _i64, _vp, _int, _int, _vp]),
     "tcu_transitive_closure": (_int, [_vp, _i64, _i64]),
     "tcu_transitive_closure_ex": (_int, [_vp, _i64, _i64, _int, _vp]),
+    "tcu_dft": (_int, [_vp, _vp, _vp, _i64, _i64]),
+    "tcu_dft_ex": (_int, [_vp, _vp, _vp, _i64, _i64, _int, _vp]),
     "tcu_calls": (_i64, []),
     "tcu_square_calls": (_i64, []),
     "tcu_work": (_i64, []),
@@ -299,6 +302,35 @@ def tcu_transitive_closure_ex(X, n: int, ld: int, s: int, stream_ptr: int | None
     st = _stream_ptr(dev) if stream_ptr is None else stream_ptr
     _check(lib().tcu_transitive_closure_ex(px or None, int(n), int(ld), int(s), st),
            "tcu_transitive_closure_ex")
+
+
+def _dft_args(where, x, y, work, n, batch):
+    import torch
+    for name, t in (("x", x), ("y", y)):
+        if t.dtype != torch.complex64:
+            raise ValueError(f"{where}: {name} must be complex64")
+    tensors = [x, y] + ([work] if work is not None else [])
+    dev, ptrs = _marshal(where, tensors, [n * batch] * len(tensors))
+    if work is not None and work.dtype != torch.complex64:
+        raise ValueError(f"{where}: work must be complex64")
+    pw = ptrs[2] if work is not None else None
+    return dev, (ptrs[0] or None), (ptrs[1] or None), (pw or None)
+
+
+def tcu_dft(x, y, work, n: int, batch: int) -> None:
+    """Theorem 7: y[b] = DFT(x[b]) for b < batch (complex64 tensors of
+    batch * n elements); work is scratch of the same size (None if n <= s)."""
+    dev, px, py, pw = _dft_args("tcu_dft", x, y, work, n, batch)
+    L = lib()
+    _check(L.tcu_set_stream(_stream_ptr(dev)), "tcu_dft")
+    _check(L.tcu_dft(px, py, pw, int(n), int(batch)), "tcu_dft")
+
+
+def tcu_dft_ex(x, y, work, n: int, batch: int, s: int, stream_ptr: int | None = None) -> None:
+    """Stateless DFT (unit size and stream as arguments)."""
+    dev, px, py, pw = _dft_args("tcu_dft_ex", x, y, work, n, batch)
+    st = _stream_ptr(dev) if stream_ptr is None else stream_ptr
+    _check(lib().tcu_dft_ex(px, py, pw, int(n), int(batch), int(s), st), "tcu_dft_ex")
 
 
 # --------------------------------------------------------- cost accounting
