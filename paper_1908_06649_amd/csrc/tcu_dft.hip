@@ -51,18 +51,35 @@ __device__ __forceinline__ f32x2 twiddle(int64_t m, int64_t N) {
   return f32x2{c, -s};
 }
 
+// Complex product of two (re, im) pairs.
+__device__ __forceinline__ f32x2 cmul(f32x2 a, f32x2 b) {
+  return f32x2{a[0] * b[0] - a[1] * b[1], a[0] * b[1] + a[1] * b[0]};
+}
+
+// One level.  n, R, P, N_t are powers of two and enter as their base-2
+// logarithms; ntrans = batch * n / R transforms, 16 per wave step.
 template <int S>
 __global__ __launch_bounds__(kDftThreads) void dft_level_kernel(
-    const f32x2 *__restrict__ src, f32x2 *__restrict__ dst, int64_t n, int R, int64_t P,
-    int64_t Nt, int64_t ntrans) {
+    const f32x2 *__restrict__ src, f32x2 *__restrict__ dst, int lg_n, int lg_r, int lg_p,
+    int64_t ntrans) {
   constexpr int kRun = S == 32 ? 8 : 4;   // contracted elements per lane
   constexpr int kH = S / 16;              // 16-frequency halves
   constexpr int kWords = kRun / 2;
   typedef typename std::conditional<kRun == 8, u32x4, u32x2>::type Run;
+  __shared__ f32x2 wtab[S];               // w_R^m, m < R
+
+  const int R = 1 << lg_r;
+  const int lg_pv = lg_n - lg_r;          // log2 of the transforms per vector
+  const int lg_nt = lg_n - lg_p;          // log2 N_t
+  const int64_t nt_mask = ((int64_t)1 << lg_nt) - 1;
+  const bool last = lg_nt == lg_r;        // N_t = R: no twiddles
+  const bool contiguous = lg_p == 0 && R >= 4;   // a lane's 4 outputs are adjacent
+
+  if (threadIdx.x < (unsigned)R) wtab[threadIdx.x] = twiddle(threadIdx.x, R);
+  __syncthreads();
 
   const int lane = threadIdx.x & 63;
   const int r = lane & 15, g = lane >> 4;
-  const int64_t per_vec = n / R;          // transforms per vector
 
   // Weights operand: row k = 16h + r, contracted run j = kRun g + e, value
   // w_R^(j k) (zero outside R x R), as hi/lo words; -Wi for the real part.
@@ -74,13 +91,9 @@ __global__ __launch_bounds__(kDftThreads) void dft_level_kernel(
 #pragma unroll
     for (int e = 0; e < kRun; ++e) {
       const int j = kRun * g + e;
-      if (j < R && k < R) {
-        const f32x2 w = twiddle((int64_t)((j * k) % R), R);
-        cr[e] = w[0];
-        ci[e] = w[1];
-      } else {
-        cr[e] = ci[e] = 0.f;
-      }
+      const f32x2 w = (j < R && k < R) ? wtab[(j * k) & (R - 1)] : f32x2{0.f, 0.f};
+      cr[e] = w[0];
+      ci[e] = w[1];
     }
 #pragma unroll
     for (int q = 0; q < kWords; ++q) {
@@ -98,20 +111,20 @@ __global__ __launch_bounds__(kDftThreads) void dft_level_kernel(
 
   const int64_t wave = (int64_t)blockIdx.x * (kDftThreads / 64) + (threadIdx.x >> 6);
   const int64_t nwaves = (int64_t)gridDim.x * (kDftThreads / 64);
-  const int64_t nchunks = (ntrans + 15) / 16;
+  const int64_t nchunks = (ntrans + 15) >> 4;
   for (int64_t chunk = wave; chunk < nchunks; chunk += nwaves) {
     const int64_t tr = chunk * 16 + r;   // this lane's transform
     const bool live = tr < ntrans;
-    const int64_t b = live ? tr / per_vec : 0;
-    const int64_t c = live ? tr - b * per_vec : 0;
-    const f32x2 *vin = src + b * n;
+    const int64_t b = live ? tr >> lg_pv : 0;
+    const int64_t c = live ? tr & (((int64_t)1 << lg_pv) - 1) : 0;
+    const f32x2 *vin = src + (b << lg_n) + c;
     // data: a[j], j = kRun g + e, as hi/lo words of the real and imaginary parts
     float xr[kRun], xi[kRun];
 #pragma unroll
     for (int e = 0; e < kRun; ++e) {
       const int j = kRun * g + e;
       f32x2 v = {0.f, 0.f};
-      if (live && j < R) v = vin[(int64_t)j * per_vec + c];
+      if (live && j < R) v = vin[(int64_t)j << lg_pv];
       xr[e] = v[0];
       xi[e] = v[1];
     }
@@ -126,8 +139,10 @@ __global__ __launch_bounds__(kDftThreads) void dft_level_kernel(
       xi_h[q] = hi;
       xi_l[q] = lo;
     }
-    const int64_t J = c / P, K = c - J * P;
-    f32x2 *vout = dst + b * n;
+    const int64_t J = c >> lg_p, K = c & (((int64_t)1 << lg_p) - 1);
+    f32x2 *vout = dst + (b << lg_n) + ((J << lg_r) << lg_p) + K;
+    // twiddle w_(N_t)^(J k) for k = k0 + i: w^(J k0) times step^i, step = w^J
+    const f32x2 step = last ? f32x2{1.f, 0.f} : twiddle(J & nt_mask, (int64_t)1 << lg_nt);
 #pragma unroll
     for (int h = 0; h < kH; ++h) {
       f32x4 re = {0.f, 0.f, 0.f, 0.f}, im = {0.f, 0.f, 0.f, 0.f};
@@ -149,20 +164,36 @@ __global__ __launch_bounds__(kDftThreads) void dft_level_kernel(
       im = mma(wr_h[h], xi_h, im);
       im = mma(wr_h[h], xi_l, im);
       im = mma(wr_l[h], xi_h, im);
-      if (!live) continue;
+      const int k0 = 16 * h + 4 * g;
+      if (!live || k0 >= R) continue;
+      f32x2 y[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int k = 16 * h + 4 * g + i;
-        if (k >= R) continue;
-        f32x2 y = {re[i], im[i]};
-        if (Nt != R) {   // twiddle w_(N_t)^(J k) (1 on the last level)
-          const f32x2 w = twiddle((J * k) & (Nt - 1), Nt);
-          y = f32x2{y[0] * w[0] - y[1] * w[1], y[0] * w[1] + y[1] * w[0]};
+      for (int i = 0; i < 4; ++i) y[i] = f32x2{re[i], im[i]};
+      if (!last) {
+        f32x2 w = twiddle((J * k0) & nt_mask, (int64_t)1 << lg_nt);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          y[i] = cmul(y[i], w);
+          if (i < 3) w = cmul(w, step);
         }
-        vout[(J * R + k) * P + K] = y;
+      }
+      if (contiguous) {   // outputs k0 .. k0+3 of transform J: 32 adjacent bytes
+        f32x4 *o = (f32x4 *)(vout + k0);
+        o[0] = f32x4{y[0][0], y[0][1], y[1][0], y[1][1]};
+        o[1] = f32x4{y[2][0], y[2][1], y[3][0], y[3][1]};
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (k0 + i < R) vout[(int64_t)(k0 + i) << lg_p] = y[i];
       }
     }
   }
+}
+
+int ilog2(int64_t v) {
+  int l = 0;
+  while (((int64_t)1 << l) < v) ++l;
+  return l;
 }
 
 template <int S>
@@ -174,7 +205,7 @@ hipError_t launch_level(const f32x2 *src, f32x2 *dst, int64_t n, int R, int64_t 
   const int64_t cap = (int64_t)num_cus * 8;
   const int blocks = (int)(want < cap ? want : cap);
   hipLaunchKernelGGL((dft_level_kernel<S>), dim3(blocks), dim3(kDftThreads), 0, stream, src, dst,
-                     n, R, P, n / P, ntrans);
+                     ilog2(n), ilog2(R), ilog2(P), ntrans);
   return hipGetLastError();
 }
 
