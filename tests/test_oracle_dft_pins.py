@@ -91,7 +91,12 @@ def _mutants():
     def unnormalized_half(x):
         return oracle.dft_direct(x) / 2
 
-    return [conj_sign, off_by_one, unnormalized_half]
+    def wrong_base(x):                                          # w = exp(-2 pi i / (n + 1))
+        n = x.shape[-1]
+        jk = np.outer(np.arange(n), np.arange(n))
+        return x @ np.exp(-2j * np.pi * jk / (n + 1))
+
+    return [conj_sign, off_by_one, unnormalized_half, wrong_base]
 
 
 def test_pins_catch_planted_mistakes():
