@@ -100,6 +100,15 @@ def counted_traffic(name: str, kind: str):
         return None
 
 
+def dft_levels(n: int, s: int) -> int:
+    """Cooley-Tukey levels of radix s (the last of radix <= s) for length n."""
+    levels, m = 1, s
+    while m < n:
+        m *= s
+        levels += 1
+    return levels
+
+
 def algorithmic(spec: dict):
     """(work per call in flop/op, bytes per call) that the method must do."""
     from paper_1908_06649_amd import inputs
@@ -110,12 +119,8 @@ def algorithmic(spec: dict):
         return 2.0 * n * s * s, n * s * ib + s * s * ib + n * s * ob
     del inputs
     if spec["kind"] == "dft":
-        n, b, s = spec["n"], spec["batch"], spec["s"]
-        levels, m = 1, s
-        while m < n:
-            m *= s
-            levels += 1
-        return 5.0 * b * n * math.log2(n), levels * 2 * 8 * b * n
+        n, b = spec["n"], spec["batch"]
+        return 5.0 * b * n * math.log2(n), dft_levels(n, spec["s"]) * 2 * 8 * b * n
     if spec["kind"] == "tc":
         # per pivot band of up to 256 vertices: the D update reads and writes
         # every off-band entry once, the panel updates their band entries
@@ -252,7 +257,8 @@ def measure(name: str, steps: int, warmup: int) -> dict:
                                  "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS,
                                  "traffic": counted_traffic(name, kind)},
                     "gflops_5nlogn": flops / (ms * 1e-3) / 1e9,
-                    "algorithmic_bytes": nbytes})
+                    "launches_per_call": dft_levels(sp["n"], sp["s"]),
+                    "algorithmic_bytes_per_launch": nbytes / dft_levels(sp["n"], sp["s"])})
     elif kind == "tc":
         gbs = nbytes / (ms * 1e-3) / 1e9
         out.update({"value": gbs, "unit": "GB/s",
@@ -497,8 +503,9 @@ def main() -> int:
             r = measure(name, args.steps, max(args.warmup, 5))
             r.pop("_workload")
             dft[name] = {k: r[k] for k in ("value", "unit", "ms_per_call", "roofline",
-                                           "gflops_5nlogn", "calls", "square_calls",
-                                           "model_work")}
+                                           "gflops_5nlogn", "launches_per_call",
+                                           "algorithmic_bytes_per_launch", "calls",
+                                           "square_calls", "model_work")}
             torch.cuda.empty_cache()
         result["dft"] = dft
     result["cost_model"] = cost
