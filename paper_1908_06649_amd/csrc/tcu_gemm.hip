@@ -590,6 +590,148 @@ gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restr
   }
 }
 
+// ---------------------------------------------------------------------------
+// Small-tile kernel for 16-bit inputs (M, N multiples of 64, K a multiple of
+// one 128-byte stage): 64 x 64 output tiles, 4 waves of 32 x 32, and a ring
+// of kStages LDS stages filled by direct DMA loads kStages - 1 stages ahead.
+// Products with few tiles and a long K per tile (N = 1024: 256 tiles with
+// K = 1024 each) are latency-bound on a register-staged double buffer, which
+// exposes one L2 round trip per K step; the ring keeps kStages - 1 stages of
+// every workgroup in flight instead.
+//   * A stage of A: 64 rows x 128 bytes as four 2 KiB blocks of 16 rows,
+//     chunk-major, so a fragment read is a linear ds_read_b128.
+//   * A stage of B: 64 k-rows x 128 bytes (64 columns), row-major, 16-byte
+//     chunks XOR-swizzled by bits 1 and 3 of the row, so that the 32 lanes
+//     of one ds_read_b64_tr_b16 pass (8 rows, 32 bytes each) hit distinct
+//     banks.
+//   * Wave w loads A block w and B rows 16w .. 16w+15 of every stage (four
+//     1 KiB DMA instructions), and computes rows 32(w/2) .., columns
+//     32(w%2) .. of the tile.
+// ---------------------------------------------------------------------------
+constexpr int kRingKB = 128;                    // bytes of K per stage
+constexpr int kRingHalf = 64 * kRingKB;         // 8 KiB per operand per stage
+
+__device__ __forceinline__ int ring_b_swz(int k) {
+  return (((k >> 1) & 1) << 1) | (((k >> 3) & 1) << 2);
+}
+
+// Wait until at most 4 * min(later, kMax) of this wave's DMA loads are in
+// flight (and its LDS reads returned), then barrier.
+template <int kMax>
+__device__ __forceinline__ void ring_wait(int later) {
+  if constexpr (kMax == 0) {
+    vm_wait_barrier<0>();
+  } else {
+    if (later >= kMax)
+      vm_wait_barrier<4 * kMax>();
+    else
+      ring_wait<kMax - 1>(later);
+  }
+}
+
+template <int DT, int kStages>
+__global__ __launch_bounds__(256) void gemm_ring_kernel(
+    const unsigned char *__restrict__ A, const unsigned char *__restrict__ B,
+    unsigned char *__restrict__ C, int K, int64_t lda, int64_t ldb, int64_t ldc, int accum,
+    int tiles_m, int tiles_n) {
+  static_assert(in_bytes(DT) == 2, "16-bit inputs");
+  static_assert(kStages >= 2 && 4 * (kStages - 2) <= 63, "vmcnt range");
+  constexpr int OB = out_bytes(DT);
+  constexpr int KE = kRingKB / 2;               // contracted elements per stage
+  __shared__ __attribute__((aligned(1024))) unsigned char sA[kStages * kRingHalf];
+  __shared__ __attribute__((aligned(1024))) unsigned char sB[kStages * kRingHalf];
+
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = w >> 1, wn = w & 1;
+  const int r = lane & 15, g = lane >> 4;
+  int tm, tn;
+  map_tile(blockIdx.x, tiles_m, tiles_n, tm, tn);
+  const int m0 = tm * 64, n0 = tn * 64;
+  const int64_t lda_b = lda * 2, ldb_b = ldb * 2, ldc_b = ldc * OB;
+  const int nk = K / KE;
+
+  // DMA share of wave w (wave-uniform bases, per-lane 32-bit offsets).
+  const unsigned char *abase = A + (int64_t)(m0 + 16 * w) * lda_b;
+  const unsigned char *bbase = B + (int64_t)(16 * w) * ldb_b + (int64_t)n0 * 2;
+  unsigned aoff[2], boff[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    aoff[h] = (unsigned)((lane & 15) * lda_b) + 16u * (4 * h + (lane >> 4));
+    const int krow = 8 * h + (lane >> 3);
+    boff[h] = (unsigned)(krow * ldb_b) + 16u * ((lane & 7) ^ ring_b_swz(16 * w + krow));
+  }
+  const unsigned a_lds = lds_addr(sA) + w * 2048, b_lds = lds_addr(sB) + w * 2048;
+  auto issue = [&](int slot, int t) {
+    const unsigned char *ga = abase + (int64_t)t * kRingKB;
+    const unsigned char *gb = bbase + (int64_t)t * KE * ldb_b;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) dma_lds16_saddr(ga, aoff[h], a_lds + slot * kRingHalf + h * 1024);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) dma_lds16_saddr(gb, boff[h], b_lds + slot * kRingHalf + h * 1024);
+  };
+
+  // Fragment offsets within a stage: A rows 32 wm .., B^T columns 32 wn ..
+  const int x_off = wm * 2 * 2048 + 16 * lane;
+  int w_off[2];
+#pragma unroll
+  for (int fn = 0; fn < 2; ++fn) {
+    const int n = wn * 32 + fn * 16 + 4 * (r & 3);
+    const int k0 = 8 * g + (r >> 2);
+    w_off[fn] = k0 * kRingKB + 16 * ((n >> 3) ^ ring_b_swz(k0)) + ((2 * n) & 15);
+  }
+
+  f32x4 acc[2][2];
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int s0 = 0; s0 < kStages - 1; ++s0)
+    if (s0 < nk) issue(s0, s0);
+  int slot = 0;
+  for (int t = 0; t < nk; ++t) {
+    // This wave's loads of stage t done (those of the stages after it may
+    // stay in flight); the barrier makes every wave's share visible and
+    // ensures all waves finished reading stage t-1, whose slot is refilled.
+    const int later = nk - 1 - t < kStages - 2 ? nk - 1 - t : kStages - 2;
+    ring_wait<kStages - 2>(later);
+    const int refill = t + kStages - 1;
+    if (refill < nk) issue(slot == 0 ? kStages - 1 : slot - 1, refill);
+    const unsigned char *sa = sA + slot * kRingHalf;
+    const unsigned char *sb = sB + slot * kRingHalf;
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      u32x4 xf[2], wf[2];
+#pragma unroll
+      for (int fm = 0; fm < 2; ++fm) xf[fm] = *(const u32x4 *)(sa + x_off + fm * 2048 + kk * 1024);
+#pragma unroll
+      for (int fn = 0; fn < 2; ++fn) {
+        const u32x2 w0 = lds_read_tr16(sb + w_off[fn] + kk * 32 * kRingKB);
+        const u32x2 w1 = lds_read_tr16(sb + w_off[fn] + kk * 32 * kRingKB + 4 * kRingKB);
+        wf[fn] = u32x4{w0[0], w0[1], w1[0], w1[1]};
+      }
+#pragma unroll
+      for (int fn = 0; fn < 2; ++fn)
+#pragma unroll
+        for (int fm = 0; fm < 2; ++fm) acc[fn][fm] = mfma_k32(DT, wf[fn], xf[fm], acc[fn][fm]);
+    }
+    slot = slot + 1 == kStages ? 0 : slot + 1;
+  }
+
+  // Epilogue: lane holds C[row][col .. col+3] of every accumulator block.
+#pragma unroll
+  for (int fn = 0; fn < 2; ++fn) {
+#pragma unroll
+    for (int fm = 0; fm < 2; ++fm) {
+      const int row = m0 + wm * 32 + fm * 16 + r;
+      const int col = n0 + wn * 32 + fn * 16 + 4 * g;
+      store_out4<DT, true>(C + (int64_t)row * ldc_b + (int64_t)col * OB, acc[fn][fm], 4,
+                           accum != 0);
+    }
+  }
+}
+
 // Zero the rows x row_bytes view at C (row pitch ldc_b bytes; row_bytes and
 // ldc_b multiples of 16): the starting value of a split-K product that
 // overwrites C.
@@ -637,12 +779,13 @@ hipError_t launch_bool(const unsigned char *A, const unsigned char *B, unsigned 
 // Kernel selection: TCU_GEMM_KERNEL=fast forces the full-tile (ping-pong)
 // kernel wherever its shape conditions hold, =general forces the general
 // kernel; unset or =auto picks by size.
-enum class GemmPath { kAuto, kFast, kGeneral };
+enum class GemmPath { kAuto, kFast, kGeneral, kRing };
 GemmPath gemm_path() {
   const char *v = std::getenv("TCU_GEMM_KERNEL");
   if (!v) return GemmPath::kAuto;
   if (!std::strcmp(v, "fast")) return GemmPath::kFast;
   if (!std::strcmp(v, "general")) return GemmPath::kGeneral;
+  if (!std::strcmp(v, "ring")) return GemmPath::kRing;
   return GemmPath::kAuto;
 }
 
@@ -701,9 +844,26 @@ hipError_t launch_dt(const RectArgs &a, hipStream_t stream, int num_cus) {
   }
   // Element-wise operand access (pitches not multiples of 16 bytes).
   if (!vec) return launch_cfg<DT, 64, 64, 2, 2, false>(a, stream);
+  const int64_t mid_tiles = ((a.M + 127) / 128) * ((a.N + 127) / 128);
+  // The small-tile ring kernel: 16-bit inputs, whole 64 x 64 tiles and
+  // 128-byte K stages, where the general kernel would take 64 x 64 tiles
+  // (or where forced, TCU_GEMM_KERNEL=ring).
+  if constexpr (ES == 2) {
+    const bool ring_ok = path != GemmPath::kGeneral && path != GemmPath::kFast &&
+                         a.M % 64 == 0 && a.N % 64 == 0 && a.K % 64 == 0 && a.K > 0 &&
+                         16 * a.lda * ES < ((int64_t)1 << 32) &&
+                         16 * a.ldb * ES < ((int64_t)1 << 32);
+    if (ring_ok && (path == GemmPath::kRing || mid_tiles < num_cus)) {
+      const int tm = (int)(a.M / 64), tn = (int)(a.N / 64);
+      hipLaunchKernelGGL((gemm_ring_kernel<DT, 8>), dim3(tm * tn), dim3(256), 0, stream,
+                         (const unsigned char *)a.A, (const unsigned char *)a.B,
+                         (unsigned char *)a.C, (int)a.K, a.lda, a.ldb, a.ldc, a.accum ? 1 : 0,
+                         tm, tn);
+      return hipGetLastError();
+    }
+  }
   // Otherwise the largest tiles that still give every CU a workgroup.
   if (big_tiles >= num_cus) return launch_cfg<DT, 256, 256, 2, 2, true>(a, stream);
-  const int64_t mid_tiles = ((a.M + 127) / 128) * ((a.N + 127) / 128);
   if (mid_tiles >= num_cus) return launch_cfg<DT, 128, 128, 2, 2, true>(a, stream);
   return launch_cfg<DT, 64, 64, 2, 2, true>(a, stream);
 }

@@ -125,10 +125,11 @@ def test_workload_i8_N8192_s32_sampled():
     compare.check("i8", "i32", inputs.bits(A), inputs.bits(B), got[rows], rows=rows)
 
 
-# Both kernels of the product on sizes where either applies (N % 256 == 0):
-# the full-tile kernel (DMA-fed LDS ring, transposing reads) and the general
-# one (register-staged, predicated tails).
-@pytest.mark.parametrize("path", ["fast", "general"])
+# Every kernel of the product on sizes where it applies (N % 256 == 0): the
+# full-tile kernel (DMA-fed LDS ring, transposing reads), the general one
+# (register-staged, predicated tails) and the small-tile ring kernel (16-bit
+# inputs; int8 falls back to the general kernel under "ring").
+@pytest.mark.parametrize("path", ["fast", "general", "ring"])
 @pytest.mark.parametrize("din,dout", DTYPES)
 @pytest.mark.parametrize("N,s", [(256, 16), (512, 32), (1280, 32)])
 def test_kernel_paths(monkeypatch, path, din, dout, N, s):
@@ -138,7 +139,7 @@ def test_kernel_paths(monkeypatch, path, din, dout, N, s):
     compare.check(din, dout, inputs.bits(A), inputs.bits(B), got)
 
 
-@pytest.mark.parametrize("path", ["fast", "general"])
+@pytest.mark.parametrize("path", ["fast", "general", "ring"])
 @pytest.mark.parametrize("din,dout", DTYPES)
 def test_kernel_paths_identity_permutation(monkeypatch, path, din, dout):
     monkeypatch.setenv("TCU_GEMM_KERNEL", path)

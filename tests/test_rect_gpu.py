@@ -81,6 +81,23 @@ def test_rect_full_tiles(M, K, N, din, out, accumulate, kernel, monkeypatch):
     run_and_check(M, K, N, din, out, 32, "padded", accumulate, seed=M + K + N)
 
 
+# Whole 64 x 64 tiles and 128-byte K stages with 16-bit inputs: the
+# small-tile ring kernel, forced, from one tile and one stage to long K
+# (many refills of its 8-slot ring) and to more tiles than CUs.
+RING = [(64, 64, 64), (64, 128, 192), (192, 448, 128), (320, 960, 128), (128, 4096, 64),
+        (1024, 1024, 1024), (2048, 192, 2112)]
+
+
+@pytest.mark.parametrize("pitch", ["contiguous", "padded"])
+@pytest.mark.parametrize("accumulate", [False, True])
+@pytest.mark.parametrize("din,out", PAIRS[:3])
+@pytest.mark.parametrize("M,K,N", RING)
+def test_rect_ring_kernel(M, K, N, din, out, accumulate, pitch, monkeypatch):
+    monkeypatch.setenv("TCU_GEMM_KERNEL", "ring")
+    s = 32 if din == "bf16" else 16
+    run_and_check(M, K, N, din, out, s, pitch, accumulate, seed=M + 5 * K + 11 * N)
+
+
 @pytest.mark.parametrize("din,out", PAIRS)
 @pytest.mark.parametrize("accumulate", [False, True])
 def test_rect_full_tiles_many_per_workgroup(din, out, accumulate, monkeypatch):
