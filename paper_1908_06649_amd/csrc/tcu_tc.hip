@@ -88,11 +88,20 @@ __device__ __forceinline__ unsigned quad_broadcast(unsigned v, int h) {
 //     pivots k it has an edge to, and ORs in the published rows of R_i.
 // That is the iterative algorithm's 32 steps over K: a vertex reaches v
 // through K exactly when some pivot it reaches through K has an edge to v.
+// Both unions over a 32-bit set are taken 4 bits at a time from tables of
+// all 16 unions of 4 consecutive pivots' words (8 lookups instead of 32
+// masked terms): tab1 over T*, tab2 over each word of the published rows.
+// A wave's lookups into tab2 touch the regions of 4 words at once; regions
+// kTab2Pitch = 136 words apart start 8 banks further on per word, so the
+// four regions (even words) fall on disjoint 16-bank windows and a lookup
+// is conflict-free (16 subsets of one region lie in 16 distinct banks).
 template <bool kVec>
 __global__ __launch_bounds__(1024) void tc_diag_kernel(unsigned char *__restrict__ D, int64_t ld,
                                                        int Bk) {
   __shared__ __attribute__((aligned(16))) unsigned krow[32][kWordsPerRow];
-  __shared__ unsigned tstar[32];
+  __shared__ unsigned tab1[8 * 16];                  // [group][subset]
+  constexpr int kTab2Pitch = 8 * 16 + 8;
+  __shared__ unsigned tab2[kWordsPerRow * kTab2Pitch];   // [word][group][subset]
   const int t = threadIdx.x;
   const int i = t >> 2;              // row
   const int w0 = 2 * (t & 3);        // this thread's words w0, w0 + 1 of row i
@@ -129,16 +138,35 @@ __global__ __launch_bounds__(1024) void tc_diag_kernel(unsigned char *__restrict
       krow[i - 32 * sb][w0 + 1] = row[1];
     }
     __syncthreads();
-    // (Pivots past nk have zero rows and no bits in kmask, so the loops
-    // below run all 32 steps, fully unrolled, with no effect from them.)
-    if (t < 32) {
-      unsigned tk = krow[t][sb] & kmask;
+    // (Pivots past nk have zero rows and no bits in kmask: they add nothing.)
+    if (t < 64) {
+      // wave 0: lanes 0..31 close the pivot block; then tab1 from T*.
+      unsigned tk = t < 32 ? krow[t][sb] & kmask : 0u;
 #pragma unroll
       for (int kk = 0; kk < 32; ++kk) {
         const unsigned pivot = (unsigned)__builtin_amdgcn_readlane((int)tk, kk);
         tk |= pivot & (0u - ((tk >> kk) & 1u));
       }
-      tstar[t] = tk | (1u << t);
+      const unsigned tstar = t < 32 ? (tk | (1u << t)) : 0u;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int e = t + 64 * h, grp = e >> 4, m = e & 15;
+        unsigned v = 0;
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+          const unsigned x = (unsigned)__shfl((int)tstar, 4 * grp + b, 64);
+          v |= x & (0u - ((unsigned)(m >> b) & 1u));
+        }
+        tab1[e] = v;
+      }
+    }
+    {
+      // tab2[w][grp][m] = union of word w of the published rows 4 grp + b, b in m
+      const int w = t >> 7, grp = (t >> 4) & 7, m = t & 15;
+      unsigned v = 0;
+#pragma unroll
+      for (int b = 0; b < 4; ++b) v |= krow[4 * grp + b][w] & (0u - ((unsigned)(m >> b) & 1u));
+      tab2[w * kTab2Pitch + (t & 127)] = v;
     }
     __syncthreads();
     // word sb of row i, from the quad lane that holds it
@@ -146,15 +174,17 @@ __global__ __launch_bounds__(1024) void tc_diag_kernel(unsigned char *__restrict
     const unsigned edges = wsb & kmask;
     unsigned reach = 0;
 #pragma unroll
-    for (int kk = 0; kk < 32; ++kk) reach |= tstar[kk] & (0u - ((edges >> kk) & 1u));
+    for (int grp = 0; grp < 8; ++grp) reach |= tab1[16 * grp + ((edges >> (4 * grp)) & 15u)];
     reach &= kmask;
 #pragma unroll
-    for (int kk = 0; kk < 32; ++kk) {
-      const unsigned m = 0u - ((reach >> kk) & 1u);
-      row[0] |= krow[kk][w0] & m;
-      row[1] |= krow[kk][w0 + 1] & m;
+    for (int q = 0; q < 2; ++q) {
+      const unsigned *t2 = tab2 + kTab2Pitch * (w0 + q);
+      unsigned add = 0;
+#pragma unroll
+      for (int grp = 0; grp < 8; ++grp) add |= t2[16 * grp + ((reach >> (4 * grp)) & 15u)];
+      row[q] |= add;
     }
-    __syncthreads();   // krow and tstar are rewritten by the next sub-band
+    __syncthreads();   // krow and the tables are rewritten by the next sub-band
   }
   // bits -> bytes
   if (i < Bk) {
