@@ -104,11 +104,15 @@ int validate_gemm(const void *A, const void *B, const void *C, int64_t N, int s,
 }
 
 // Bytes from the base of an R x C view with row pitch ld (elements of es
-// bytes) to one past its last element; 0 for an empty view.  Inputs are
-// bounded (R, C <= 2^30, ld < 2^40) so the product cannot overflow.
+// bytes) to one past its last element; 0 for an empty view.  Formed in
+// 128-bit arithmetic and saturated at 2^62, so that no combination of
+// in-range arguments (R up to 2^30 rows of pitch up to 2^62) can wrap
+// around and pass a size check.
 int64_t view_extent(int64_t rows, int64_t cols, int64_t ld, int64_t es) {
-  if (rows == 0 || cols == 0) return 0;
-  return ((rows - 1) * ld + cols) * es;
+  if (rows <= 0 || cols <= 0) return 0;
+  const __int128 e = ((__int128)(rows - 1) * ld + cols) * es;
+  constexpr int64_t kSat = (int64_t)1 << 62;
+  return e > (__int128)kSat ? kSat : (int64_t)e;
 }
 
 // Whether two row-major views (base, rows, bytes per row, byte pitch) share
@@ -191,7 +195,8 @@ int validate_tc(const void *X, int64_t n, int64_t ld, int s) {
 int validate_dft(const void *x, const void *y, const void *work, int64_t n, int64_t batch, int s) {
   if (!unit_ok(s)) return TCU_ERR_UNSUPPORTED;
   if (n < 1 || n > TCU_MAX_DFT_N || (n & (n - 1)) != 0 || batch < 0) return TCU_ERR_SHAPE;
-  if (batch > 0 && n > ((int64_t)1 << 40) / 8 / batch) return TCU_ERR_SHAPE;
+  // batch * n * 8 bytes must stay below 2^40
+  if (batch > 0 && n > (((int64_t)1 << 40) - 1) / 8 / batch) return TCU_ERR_SHAPE;
   const int64_t bytes = batch * n * 8;
   const bool need_work = tcu::dft_levels(n, s) > 1;
   if (bytes > 0 && (!x || !y || (need_work && !work))) return TCU_ERR_NULL;

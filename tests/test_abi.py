@@ -221,6 +221,25 @@ RECT_ERRORS = [
 ]
 
 
+# Extents whose int64 product would wrap around: the validation (128-bit,
+# saturating) must see them as too large, not as small or negative sizes.
+# (Run only where no device is visible: a wrong acceptance must not reach a
+# launch.)
+RECT_OVERFLOW = [
+    (PA, 1 << 39, PB, 64, PC, 64, 1 << 30, 1, 64, 0, 16, 0),      # (M-1) lda ~ 2^69
+    (PA, 64, PB, 1 << 39, PC, 64, 64, 1 << 30, 64, 0, 16, 0),     # (K-1) ldb
+    (PA, 64, PB, 64, PC, (1 << 40) - 16, 1 << 30, 64, 64, 0, 16, 0),  # (M-1) ldc * 4
+]
+
+
+@pytest.mark.skipif(torch.cuda.device_count() > 0, reason="a HIP device is visible")
+@pytest.mark.parametrize("args", RECT_OVERFLOW)
+def test_rect_rejects_wrapping_extents(L, args):
+    L.tcu_reset_calls()
+    assert L.tcu_gemm_rect_ex(*args, None) == tcu.TCU_ERR_SHAPE
+    assert L.tcu_calls() == 0
+
+
 @pytest.mark.parametrize("args,want", RECT_ERRORS)
 def test_rect_rejects(L, args, want):
     L.tcu_reset_calls()
@@ -302,3 +321,113 @@ def test_python_rect_marshalling_errors():
     C = torch.zeros(64, 16, dtype=torch.float32)
     with pytest.raises(ValueError):          # host tensors
         tcu.tcu_gemm_rect(A, 32, B, 16, C, 16, 64, 32, 16)
+
+
+# ---- polynomial evaluation, transitive closure, DFT: argument checks ----
+
+POLY_ERRORS = [
+    # (coef, n, points, p, out, s, dtype) -> status
+    ((PA, 100, PB, 64, PC, 8, 1), tcu.TCU_ERR_UNSUPPORTED),
+    ((PA, 100, PB, 64, PC, 32, 3), tcu.TCU_ERR_UNSUPPORTED),     # int8 has no polynomial form
+    ((PA, 100, PB, 64, PC, 32, 9), tcu.TCU_ERR_UNSUPPORTED),
+    ((PA, -1, PB, 64, PC, 32, 1), tcu.TCU_ERR_SHAPE),
+    ((PA, 100, PB, -1, PC, 32, 1), tcu.TCU_ERR_SHAPE),
+    ((PA, (1 << 40) + 1, PB, 64, PC, 32, 1), tcu.TCU_ERR_SHAPE),
+    ((PA, 100, PB, (1 << 40) + 1, PC, 32, 1), tcu.TCU_ERR_SHAPE),
+    ((0, 100, PB, 64, PC, 32, 1), tcu.TCU_ERR_NULL),
+    ((PA, 100, 0, 64, PC, 32, 1), tcu.TCU_ERR_NULL),
+    ((PA, 100, PB, 64, 0, 32, 1), tcu.TCU_ERR_NULL),
+    ((PA + 8, 100, PB, 64, PC, 32, 1), tcu.TCU_ERR_ALIGN),
+    ((PA, 100, PB, 64, PC + 4, 32, 1), tcu.TCU_ERR_ALIGN),
+    ((PA, 100, PB, 64, PB + 64, 32, 1), tcu.TCU_ERR_OVERLAP),      # out over the points
+    ((PA, 100, PB, 64, PA + 192, 32, 0), tcu.TCU_ERR_OVERLAP),     # out over the coefficients
+]
+
+
+@pytest.mark.parametrize("args,want", POLY_ERRORS)
+def test_poly_rejects(L, args, want):
+    L.tcu_reset_calls()
+    assert L.tcu_poly_eval_ex(*args, None) == want
+    assert L.tcu_calls() == 0
+
+
+def test_poly_empty_needs_no_device(L):
+    """p = 0 (nothing to evaluate) succeeds before any device call; NULL
+    arrays are allowed when empty."""
+    L.tcu_reset_calls()
+    assert L.tcu_poly_eval_ex(PA, 100, 0, 0, 0, 32, 1, None) == tcu.TCU_OK
+    assert L.tcu_poly_eval_ex(0, 0, 0, 0, 0, 16, 0, None) == tcu.TCU_OK
+    assert L.tcu_calls() == 0
+
+
+TC_ERRORS = [
+    # (X, n, ld, s) -> status
+    ((PA, 64, 64, 8), tcu.TCU_ERR_UNSUPPORTED),
+    ((PA, -1, 64, 32), tcu.TCU_ERR_SHAPE),
+    ((PA, (1 << 30) + 1, (1 << 30) + 1, 32), tcu.TCU_ERR_SHAPE),
+    ((PA, 64, 63, 32), tcu.TCU_ERR_SHAPE),                         # ld < n
+    ((PA, 1 << 20, 1 << 21, 32), tcu.TCU_ERR_SHAPE),               # extent 2^41 bytes
+    ((0, 64, 64, 32), tcu.TCU_ERR_NULL),
+    ((PA + 4, 64, 64, 32), tcu.TCU_ERR_ALIGN),
+]
+
+
+@pytest.mark.parametrize("args,want", TC_ERRORS)
+def test_tc_rejects(L, args, want):
+    L.tcu_reset_calls()
+    assert L.tcu_transitive_closure_ex(*args, None) == want
+    assert L.tcu_calls() == 0
+
+
+@pytest.mark.skipif(torch.cuda.device_count() > 0, reason="a HIP device is visible")
+def test_tc_rejects_wrapping_extent(L):
+    """(n - 1) ld ~ 2^82 must read as too large, not wrap around."""
+    assert L.tcu_transitive_closure_ex(PA, 1 << 20, 1 << 62, 32, None) == tcu.TCU_ERR_SHAPE
+
+
+def test_tc_empty_needs_no_device(L):
+    L.tcu_reset_calls()
+    assert L.tcu_transitive_closure_ex(0, 0, 0, 32, None) == tcu.TCU_OK
+    assert L.tcu_calls() == 0
+
+
+DFT_ERRORS = [
+    # (x, y, work, n, batch, s) -> status
+    ((PA, PB, PC, 1024, 1, 8), tcu.TCU_ERR_UNSUPPORTED),
+    ((PA, PB, PC, 0, 1, 32), tcu.TCU_ERR_SHAPE),
+    ((PA, PB, PC, 96, 1, 32), tcu.TCU_ERR_SHAPE),                  # not a power of two
+    ((PA, PB, PC, (1 << 30) * 2, 1, 32), tcu.TCU_ERR_SHAPE),
+    ((PA, PB, PC, 1024, -1, 32), tcu.TCU_ERR_SHAPE),
+    ((PA, PB, PC, 1 << 30, 1 << 7, 32), tcu.TCU_ERR_SHAPE),        # 2^40 bytes
+    ((0, PB, PC, 1024, 1, 32), tcu.TCU_ERR_NULL),
+    ((PA, 0, PC, 1024, 1, 32), tcu.TCU_ERR_NULL),
+    ((PA, PB, 0, 1024, 1, 32), tcu.TCU_ERR_NULL),                  # two levels need work
+    ((PA + 8, PB, PC, 1024, 1, 32), tcu.TCU_ERR_ALIGN),
+    ((PA, PB, PC + 8, 1024, 1, 32), tcu.TCU_ERR_ALIGN),
+    ((PA, PA + 4096, PC, 1024, 1, 32), tcu.TCU_ERR_OVERLAP),       # y over x
+    ((PA, PB, PB + 8192 - 16, 1024, 1, 32), tcu.TCU_ERR_OVERLAP),  # work over y
+    ((PA, PB, PA, 1024, 1, 32), tcu.TCU_ERR_OVERLAP),              # work over x
+]
+
+
+@pytest.mark.parametrize("args,want", DFT_ERRORS)
+def test_dft_rejects(L, args, want):
+    L.tcu_reset_calls()
+    assert L.tcu_dft_ex(*args, None) == want
+    assert L.tcu_calls() == 0
+
+
+def test_dft_empty_batch_needs_no_device(L):
+    L.tcu_reset_calls()
+    assert L.tcu_dft_ex(0, 0, 0, 1024, 0, 32, None) == tcu.TCU_OK
+    assert L.tcu_calls() == 0
+
+
+@pytest.mark.skipif(torch.cuda.device_count() > 0, reason="a HIP device is visible")
+def test_new_entry_points_valid_arguments_without_device(L):
+    """Valid arguments get as far as the device check (one level needs no
+    work buffer)."""
+    assert L.tcu_poly_eval_ex(PA, 100, PB, 64, PC, 32, 1, None) == tcu.TCU_ERR_NO_DEVICE
+    assert L.tcu_transitive_closure_ex(PA, 64, 64, 32, None) == tcu.TCU_ERR_NO_DEVICE
+    assert L.tcu_dft_ex(PA, PB, 0, 32, 4, 32, None) == tcu.TCU_ERR_NO_DEVICE
+    assert L.tcu_dft_ex(PA, PB, PC, 1 << 20, 4, 32, None) == tcu.TCU_ERR_NO_DEVICE
