@@ -111,13 +111,11 @@ def dft_levels(n: int, s: int) -> int:
 
 def algorithmic(spec: dict):
     """(work per call in flop/op, bytes per call) that the method must do."""
-    from paper_1908_06649_amd import inputs
     ib = 1 if spec.get("dtype", "i8") == "i8" else 2
     ob = 2 if spec.get("out") == "bf16" else 4
     if spec["kind"] == "tall":
         n, s = spec["n"], spec["s"]
         return 2.0 * n * s * s, n * s * ib + s * s * ib + n * s * ob
-    del inputs
     if spec["kind"] == "dft":
         n, b = spec["n"], spec["batch"]
         return 5.0 * b * n * math.log2(n), dft_levels(n, spec["s"]) * 2 * 8 * b * n
@@ -388,9 +386,9 @@ def main() -> int:
     args = ap.parse_args()
 
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
-              "the hot path needs no collectives, and a multi-GPU run is not part of it.",
-              file=sys.stderr)
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}): the library "
+              "has no multi-GPU path (its calls need no collectives; rows shard with no "
+              "exchange).", file=sys.stderr)
         return 2
     import torch
     if not torch.cuda.is_available():
