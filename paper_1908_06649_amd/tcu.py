@@ -118,9 +118,19 @@ def _dtype_code(a_dtype, c_dtype) -> int:
         raise TcuError(TCU_ERR_UNSUPPORTED, f"dtype pair ({a_dtype}, {c_dtype})") from None
 
 
+def _check_current_device(where: str, dev) -> None:
+    """The library launches on the current HIP device: the tensors must be
+    there (select it with torch.cuda.device(...))."""
+    import torch
+    if dev.type == "cuda" and dev.index is not None and dev.index != torch.cuda.current_device():
+        raise ValueError(f"{where}: tensors are on {dev}, the current device is "
+                         f"cuda:{torch.cuda.current_device()}")
+
+
 def _marshal(where: str, tensors, numels):
-    """Check that tensors are contiguous, on one HIP device, and sized as the
-    call will read/write them; return their device pointers."""
+    """Check that tensors are contiguous, on one HIP device (the current one),
+    and sized as the call will read/write them; return their device
+    pointers."""
     dev = tensors[0].device
     ptrs = []
     for t, want in zip(tensors, numels):
@@ -131,6 +141,7 @@ def _marshal(where: str, tensors, numels):
         if t.numel() != want:
             raise ValueError(f"{where}: expected {want} elements, got {t.numel()}")
         ptrs.append(t.data_ptr())
+    _check_current_device(where, dev)
     return dev, ptrs
 
 
@@ -203,8 +214,8 @@ def tcu_gemm_ex(A, B, C, N: int, s: int, stream_ptr: int | None = None) -> None:
 
 def _marshal_views(where: str, views):
     """(tensor, rows, cols, ld) per operand: check that each is a 2-D view of
-    that shape with unit column stride and row pitch ld on one HIP device;
-    return the device and the view base pointers."""
+    that shape with unit column stride and row pitch ld on one HIP device
+    (the current one); return the device and the view base pointers."""
     dev = views[0][0].device
     ptrs = []
     for t, rows, cols, ld in views:
@@ -217,6 +228,7 @@ def _marshal_views(where: str, views):
         if rows > 1 and t.stride(0) != ld:
             raise ValueError(f"{where}: row pitch {t.stride(0)} does not match ld={ld}")
         ptrs.append(t.data_ptr())
+    _check_current_device(where, dev)
     return dev, ptrs
 
 
