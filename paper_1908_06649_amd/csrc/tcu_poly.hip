@@ -21,9 +21,10 @@
 //     matrix-core products per 16-column half (X_hi, then X_lo into the
 //     same binary32 accumulators);
 //   * lane (r, g) then holds C[point r][columns 16h + 4g + i] of the block
-//     and forms t = sum of them with weights y^(16h + 4g + i), y = x^s; the
-//     blocks are walked last to first and combined by Horner's rule in
-//     y^s (acc = acc * y^s + t) -- the final combine, never writing C;
+//     and forms t = sum over them of C y^(16h + i), y = x^s, by Horner's
+//     rule in y; the blocks are walked last to first and combined by
+//     Horner's rule in y^s (acc = acc * y^s + t), and the lane's factor
+//     y^(4g) is applied once -- the final combine, never writing C;
 //   * the four lanes holding one point add their sums (cross-lane
 //     exchange) and one stores A(x_i).
 // Coefficients past n and points past p are zero padding.  Results are
@@ -102,8 +103,7 @@ __global__ __launch_bounds__(kPolyThreads) void poly_kernel(const unsigned char 
 
   for (int64_t t0 = wave * U; t0 < nchunks; t0 += nwaves * U) {
     Run xh[U], xl[U];
-    float w[U][kH][4];
-    float acc[U], ystep[U];
+    float yv[U], y16v[U], yg[U], acc[U], ystep[U];
     // All U points first (clamped index, then a select), so the loads are
     // in flight together.
     unsigned short praw[U];
@@ -134,25 +134,18 @@ __global__ __launch_bounds__(kPolyThreads) void poly_kernel(const unsigned char 
         xh[u][q] = hi;
         xl[u][q] = lo;
       }
-      // Combine weights y^(16h + 4g + i) and the block step y^S.
+      // The combine: column c = 16h + 4g + i of a block has weight
+      // y^c = y^(4g) y^(16h) y^i, y = x^S; a lane forms its columns' sum by
+      // Horner's rule in y (and y^16 across the halves), the blocks by
+      // Horner's rule in y^S, and applies y^(4g) once at the end.  A power
+      // that only multiplies unused (zero) columns is replaced by 0, so that
+      // it cannot overflow where the polynomial does not: every power kept
+      // divides x^(n-1).
       const float y = S == 32 ? x16 * x16 : x16;
       const float y2 = y * y, y4 = y2 * y2, y8 = y4 * y4, y16 = y8 * y8;
-      const float wv = pow_group(g, y4, y8);
-#pragma unroll
-      for (int h = 0; h < kH; ++h) {
-        float v = h == 0 ? wv : wv * y16;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          w[u][h][i] = v;
-          v *= y;
-        }
-      }
-      if (ncols < S) {   // output columns past ceil(n/S) are not used
-#pragma unroll
-        for (int h = 0; h < kH; ++h)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) w[u][h][i] = 16 * h + 4 * g + i < ncols ? w[u][h][i] : 0.f;
-      }
+      yv[u] = ncols >= 2 ? y : 0.f;
+      y16v[u] = ncols > 16 ? y16 : 0.f;
+      yg[u] = 4 * g < ncols ? pow_group(g, y4, y8) : 0.f;
       ystep[u] = S == 32 ? y16 * y16 : y16;
       acc[u] = 0.f;
     }
@@ -197,8 +190,9 @@ __global__ __launch_bounds__(kPolyThreads) void poly_kernel(const unsigned char 
             d = mfma_k16(DT, wf[h], xh[u], f32x4{0.f, 0.f, 0.f, 0.f});
             d = mfma_k16(DT, wf[h], xl[u], d);
           }
-#pragma unroll
-          for (int i = 0; i < 4; ++i) t += d[i] * w[u][h][i];
+          const float th = __builtin_fmaf(
+              __builtin_fmaf(__builtin_fmaf(d[3], yv[u], d[2]), yv[u], d[1]), yv[u], d[0]);
+          t = h == 0 ? th : __builtin_fmaf(th, y16v[u], t);
         }
         // Horner over the blocks, last block first: acc = acc * y^S + t.
         acc[u] = J == nblocks - 1 ? t : acc[u] * ystep[u] + t;
@@ -207,7 +201,7 @@ __global__ __launch_bounds__(kPolyThreads) void poly_kernel(const unsigned char 
 
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      float v = acc[u];
+      float v = acc[u] * yg[u];
       v += __shfl_xor(v, 16);
       v += __shfl_xor(v, 32);
       const int64_t idx = (t0 + u) * 16 + r;
