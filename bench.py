@@ -358,7 +358,9 @@ def cpu_baseline(w: "Workload", target_s: float = 15.0) -> dict:
 
 def copy_probe() -> None:
     """A plain device copy of known size (1 GiB), for calibrating rocprofv3's
-    FETCH_SIZE / WRITE_SIZE counters."""
+    FETCH_SIZE / WRITE_SIZE counters (the first 3 copies), then timed (20
+    more, after a settle) as the rate a plain stream reaches on this GPU:
+    the practical ceiling of the HBM-bound kernels."""
     import torch
     nbytes = 1 << 30
     src = torch.empty(nbytes // 4, dtype=torch.int32, device="cuda").fill_(1)
@@ -367,7 +369,10 @@ def copy_probe() -> None:
     for _ in range(3):
         dst.copy_(src)
     torch.cuda.synchronize()
-    print(json.dumps({"copy_probe_bytes_each_way": nbytes, "copies": 3}))
+    ms = time_steps(lambda: dst.copy_(src), 20, 3)
+    print(json.dumps({"copy_probe_bytes_each_way": nbytes, "copies": 3,
+                      "timed_copies": 20, "ms_per_copy": ms,
+                      "GB_per_s_read_plus_write": 2 * nbytes / (ms * 1e-3) / 1e9}))
 
 
 def main() -> int:
