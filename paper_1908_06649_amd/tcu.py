@@ -104,37 +104,42 @@ def _check(rc: int, where: str) -> None:
         raise TcuError(rc, where)
 
 
+_DTYPES = None
+
+
 def _dtype_code(a_dtype, c_dtype) -> int:
-    import torch
-    table = {
-        (torch.float16, torch.float32): TCU_F16_F32,
-        (torch.bfloat16, torch.float32): TCU_BF16_F32,
-        (torch.bfloat16, torch.bfloat16): TCU_BF16_BF16,
-        (torch.int8, torch.int32): TCU_I8_I32,
-    }
-    try:
-        return table[(a_dtype, c_dtype)]
-    except KeyError:
-        raise TcuError(TCU_ERR_UNSUPPORTED, f"dtype pair ({a_dtype}, {c_dtype})") from None
+    global _DTYPES
+    if _DTYPES is None:
+        import torch
+        _DTYPES = {
+            (torch.float16, torch.float32): TCU_F16_F32,
+            (torch.bfloat16, torch.float32): TCU_BF16_F32,
+            (torch.bfloat16, torch.bfloat16): TCU_BF16_BF16,
+            (torch.int8, torch.int32): TCU_I8_I32,
+        }
+    code = _DTYPES.get((a_dtype, c_dtype))
+    if code is None:
+        raise TcuError(TCU_ERR_UNSUPPORTED, f"dtype pair ({a_dtype}, {c_dtype})")
+    return code
 
 
-def _check_current_device(where: str, dev) -> None:
+def _check_current_device(where: str, dev: int) -> None:
     """The library launches on the current HIP device: the tensors must be
     there (select it with torch.cuda.device(...))."""
     import torch
-    if dev.type == "cuda" and dev.index is not None and dev.index != torch.cuda.current_device():
-        raise ValueError(f"{where}: tensors are on {dev}, the current device is "
-                         f"cuda:{torch.cuda.current_device()}")
+    cur = torch.cuda.current_device()
+    if dev != cur:
+        raise ValueError(f"{where}: tensors are on cuda:{dev}, the current device is cuda:{cur}")
 
 
 def _marshal(where: str, tensors, numels):
     """Check that tensors are contiguous, on one HIP device (the current one),
-    and sized as the call will read/write them; return their device
-    pointers."""
-    dev = tensors[0].device
+    and sized as the call will read/write them; return the device index and
+    their device pointers."""
+    dev = tensors[0].get_device() if tensors[0].is_cuda else -1
     ptrs = []
     for t, want in zip(tensors, numels):
-        if t.device != dev or t.device.type != "cuda":
+        if not t.is_cuda or t.get_device() != dev:
             raise ValueError(f"{where}: all matrices must be on the same HIP device")
         if not t.is_contiguous():
             raise ValueError(f"{where}: matrices must be contiguous (row-major)")
@@ -145,9 +150,18 @@ def _marshal(where: str, tensors, numels):
     return dev, ptrs
 
 
-def _stream_ptr(dev) -> int:
-    import torch
-    return torch.cuda.current_stream(dev).cuda_stream
+_RAW_STREAM = None
+
+
+def _stream_ptr(dev: int) -> int:
+    """The current torch stream of device dev, as a hipStream_t value."""
+    global _RAW_STREAM
+    if _RAW_STREAM is None:
+        import torch
+        raw = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+        _RAW_STREAM = raw if raw is not None else (
+            lambda d: torch.cuda.current_stream(d).cuda_stream)
+    return _RAW_STREAM(dev)
 
 
 # ------------------------------------------------------------ configuration
@@ -215,11 +229,11 @@ def tcu_gemm_ex(A, B, C, N: int, s: int, stream_ptr: int | None = None) -> None:
 def _marshal_views(where: str, views):
     """(tensor, rows, cols, ld) per operand: check that each is a 2-D view of
     that shape with unit column stride and row pitch ld on one HIP device
-    (the current one); return the device and the view base pointers."""
-    dev = views[0][0].device
+    (the current one); return the device index and the view base pointers."""
+    dev = views[0][0].get_device() if views[0][0].is_cuda else -1
     ptrs = []
     for t, rows, cols, ld in views:
-        if t.device != dev or t.device.type != "cuda":
+        if not t.is_cuda or t.get_device() != dev:
             raise ValueError(f"{where}: all matrices must be on the same HIP device")
         if t.dim() != 2 or tuple(t.shape) != (rows, cols):
             raise ValueError(f"{where}: expected a {rows} x {cols} view, got {tuple(t.shape)}")
