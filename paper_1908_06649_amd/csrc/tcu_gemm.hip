@@ -564,21 +564,31 @@ gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restr
       __syncthreads();   // staging reads done before the ring is refilled
     } else {
       // Epilogue: lane holds C[row][col .. col+3] of every accumulator block.
+      auto out_ptr = [&](int fn, int fm) {
+        const int row = m0 + grp * 128 + fm * 16 + r;
+        const int col = n0 + q * 64 + fn * 16 + 4 * g;
+        return C + (int64_t)row * ldc_b + (int64_t)col * OB;
+      };
+      constexpr bool kSplittable = DT == TCU_F16_F32 || DT == TCU_BF16_F32 || DT == TCU_I8_I32;
+      if (kSplittable && nsplit > 1) {
+        // Partial tiles: consecutive atomic adds go to different rows (and
+        // so different cache lines); adds into one line serialize in L2.
+        if constexpr (kSplittable) {
 #pragma unroll
-      for (int fn = 0; fn < FN; ++fn) {
+          for (int fn = 0; fn < FN; ++fn)
 #pragma unroll
-        for (int fm = 0; fm < FM; ++fm) {
-          const int row = m0 + grp * 128 + fm * 16 + r;
-          const int col = n0 + q * 64 + fn * 16 + 4 * g;
-          unsigned char *p = C + (int64_t)row * ldc_b + (int64_t)col * OB;
-          if constexpr (DT == TCU_F16_F32 || DT == TCU_BF16_F32 || DT == TCU_I8_I32) {
-            if (nsplit > 1) {
-              atomic_add_out4<DT>(p, acc[fn][fm]);
-              continue;
-            }
-          }
-          store_out4<DT, true>(p, acc[fn][fm], 4, accum != 0);
+            for (int fm = 0; fm < FM; ++fm) atomic_add_out4<DT>(out_ptr(fn, fm), acc[fn][fm]);
         }
+      } else {
+        // Blocks fn and fn + 1 hold the two 64-byte halves of 128-byte rows
+        // of C, so they are stored back to back: a half-written line left
+        // in L2 while other stores intervene is written to memory twice
+        // (measured: 1.37x the output bytes with fn outermost, 1.006x here).
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+          for (int fn = 0; fn < FN; ++fn)
+            store_out4<DT, true>(out_ptr(fn, fm), acc[fn][fm], 4, accum != 0);
       }
     }
     // Every wave finished reading the ring at the last barrier of the loop.

@@ -119,3 +119,36 @@ def test_tc_workload(name):
     want = oracle.transitive_closure(d)
     assert np.array_equal(got, want)
     print(name, "closure density", float(want.mean()))
+
+
+def test_tc_on_side_stream_joins():
+    """On a non-default stream: once the caller's stream is synchronized (and
+    nothing else), every update of the closure has landed."""
+    n = 2048
+    d = graph(n, 1.0, 77)
+    want = oracle.transitive_closure(d)
+    st = torch.cuda.Stream()
+    X = torch.from_numpy(d).to(gu.DEV)
+    st.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(st):
+        tcu.tcu_transitive_closure(X, n, n)
+        out = torch.empty((n, n), dtype=torch.uint8, device="cpu", pin_memory=True)
+        out.copy_(X, non_blocking=True)
+    st.synchronize()
+    assert np.array_equal(out.numpy(), want)
+
+
+def test_tc_two_streams_back_to_back():
+    """Two closures enqueued on two streams without a synchronization in
+    between (they share the library's second stream and events)."""
+    n = 1536
+    ds = [graph(n, 1.2, 5), graph(n, 0.8, 6)]
+    Xs = [torch.from_numpy(d).to(gu.DEV) for d in ds]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    for st in streams:
+        st.wait_stream(torch.cuda.current_stream())
+    for X, st in zip(Xs, streams):
+        tcu.tcu_transitive_closure_ex(X, n, n, 32, st.cuda_stream)
+    torch.cuda.synchronize()
+    for X, d in zip(Xs, ds):
+        assert np.array_equal(X.cpu().numpy(), oracle.transitive_closure(d))
