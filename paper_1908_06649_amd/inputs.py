@@ -89,6 +89,47 @@ def draw(shape, dtype: str, dist: str, gen: torch.Generator) -> torch.Tensor:
     return x.to(TORCH_DTYPE[dtype])
 
 
+def draw_on(device, shape, dtype: str, dist: str, seed: int) -> torch.Tensor:
+    """As ``draw`` with torch's own generator on ``device`` (seeded): for
+    inputs too large to draw on the host and copy.  The oracle is given the
+    same stored bytes, copied back."""
+    gen = torch.Generator(device=device)
+    gen.manual_seed(seed)
+    if dtype == "i8":
+        return torch.randint(-128, 128, shape, generator=gen, dtype=torch.int8, device=device)
+    if dist == "uniform":
+        x = torch.rand(shape, generator=gen, dtype=torch.float32, device=device).mul_(2.0).sub_(1.0)
+    elif dist == "normal":
+        x = torch.randn(shape, generator=gen, dtype=torch.float32, device=device)
+    else:
+        raise ValueError(f"unknown distribution {dist!r}")
+    return x.to(TORCH_DTYPE[dtype])
+
+
+def cycle_graph(n: int, max_len: int, seed: int):
+    """A directed graph on n vertices that is a disjoint union of cycles: the
+    vertices in a random order, cut at random points into runs of 1 ..
+    max_len vertices, each run closed into a cycle (a run of one vertex is a
+    self loop).  Returns (src, dst, label) as int64 tensors: the edges, and
+    for every vertex the index of its cycle."""
+    gen = torch.Generator(device="cpu")
+    gen.manual_seed(seed)
+    order = torch.randperm(n, generator=gen)
+    lens = torch.randint(1, max_len + 1, (n,), generator=gen)
+    ends = torch.cumsum(lens, 0)
+    ends = ends[ends < n]
+    starts = torch.cat([torch.zeros(1, dtype=torch.int64), ends])
+    stops = torch.cat([ends, torch.tensor([n])])
+    src, dst = [], []
+    label = torch.empty(n, dtype=torch.int64)
+    for c, (a, b) in enumerate(zip(starts.tolist(), stops.tolist())):
+        run = order[a:b]
+        src.append(run)
+        dst.append(torch.roll(run, -1))
+        label[run] = c
+    return torch.cat(src), torch.cat(dst), label
+
+
 def shapes(spec: dict):
     """(A shape, B shape, C shape) of a workload spec."""
     if spec["kind"] == "tall":

@@ -1,0 +1,145 @@
+"""GPU parity past 2^31 elements for every entry point, through the C ABI:
+sizes whose element (or byte) offsets do not fit in 32 bits.
+
+The inputs are drawn on the device by torch's seeded generator
+(inputs.draw_on; too large to draw on the host and copy).  The oracle gets
+the same stored bytes of the sampled rows, points or vectors, copied back.
+The samples include the first rows, the rows on both sides of the
+2^31-element boundary and the last rows.  Every output buffer carries a
+guard region that must stay untouched."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import compare
+from paper_1908_06649_amd import inputs, tcu
+
+import gpu_util as gu
+
+pytestmark = pytest.mark.gpu
+
+G = 1 << 31
+
+
+@pytest.fixture(autouse=True)
+def _release_memory():
+    yield
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+def host_bits(t: torch.Tensor) -> np.ndarray:
+    return inputs.bits(t.cpu())
+
+
+def sample(n: int, boundary: int, seed: int, k: int = 256) -> np.ndarray:
+    """Sorted distinct indices < n: the first 8, 8 on each side of
+    `boundary`, the last 8 and k random ones."""
+    rng = np.random.default_rng(seed)
+    idx = np.concatenate([np.arange(8), np.arange(boundary - 8, boundary + 8),
+                          np.arange(n - 8, n), rng.integers(0, n, k)])
+    return np.unique(idx[(idx >= 0) & (idx < n)])
+
+
+@pytest.mark.parametrize("din,dout", [("bf16", "bf16"), ("i8", "i32")])
+def test_tall_beyond_2g_elements(din, dout):
+    s = 32
+    n = G // s + 4099                       # n s = 2^31 + 131168 elements
+    A = inputs.draw_on(gu.DEV, (n, s), din, "int8" if din == "i8" else "normal", seed=31)
+    gen = torch.Generator().manual_seed(32)
+    B = inputs.draw((s, s), din, "int8" if din == "i8" else "normal", gen)
+    buf, C = gu.sentinel_buffer(n * s, gu.out_dtype(dout))
+    tcu.tcu_set_unit(s)
+    tcu.tcu_mm_tall(A, n, s, B.to(gu.DEV), C.view(n, s))
+    torch.cuda.synchronize()
+    assert gu.guard_intact(buf, n * s), "wrote past the end of C"
+    rows = sample(n, G // s, seed=1)
+    ridx = torch.from_numpy(rows).to(gu.DEV)
+    got = gu.to_np(C.view(n, s).index_select(0, ridx))
+    rep = compare.check(din, dout, host_bits(A.index_select(0, ridx)), inputs.bits(B), got)
+    print(din, dout, n, rep)
+
+
+@pytest.mark.parametrize("din,dout", [("bf16", "f32"), ("i8", "i32")])
+def test_gemm_beyond_2g_elements(din, dout):
+    N, s = 1 << 16, 32                      # N^2 = 2^32 elements per matrix
+    dist = "int8" if din == "i8" else "normal"
+    A = inputs.draw_on(gu.DEV, (N, N), din, dist, seed=41)
+    B = inputs.draw_on(gu.DEV, (N, N), din, dist, seed=42)
+    buf, C = gu.sentinel_buffer(N * N, gu.out_dtype(dout))
+    tcu.tcu_set_unit(s)
+    tcu.tcu_gemm(A, B, C.view(N, N), N)
+    torch.cuda.synchronize()
+    assert gu.guard_intact(buf, N * N), "wrote past the end of C"
+    rows = sample(N, G // N, seed=2, k=24)
+    cols = sample(N, N // 2, seed=3, k=24)
+    ridx = torch.from_numpy(rows).to(gu.DEV)
+    cidx = torch.from_numpy(cols).to(gu.DEV)
+    got = gu.to_np(C.view(N, N).index_select(0, ridx).index_select(1, cidx))
+    a_rows = host_bits(A.index_select(0, ridx))
+    b_cols = host_bits(B.index_select(1, cidx))
+    rep = compare.check(din, dout, a_rows, b_cols, got)
+    print(din, dout, N, rep)
+
+
+def test_poly_beyond_2g_points():
+    s, n = 32, 4096
+    p = G + 37
+    gen = torch.Generator().manual_seed(51)
+    coef = inputs.draw((n,), "bf16", "normal", gen)
+    pts = inputs.draw_on(gu.DEV, (p,), "bf16", "uniform", seed=52)
+    buf, out = gu.sentinel_buffer(p, torch.float32)
+    tcu.tcu_set_unit(s)
+    tcu.tcu_poly_eval(coef.to(gu.DEV), n, pts, p, out)
+    torch.cuda.synchronize()
+    assert gu.guard_intact(buf, p), "wrote past the end of the output"
+    idx = torch.from_numpy(sample(p, G, seed=4)).to(gu.DEV)
+    got = out.index_select(0, idx).cpu().numpy()
+    rep = compare.check_poly("bf16", "f32", inputs.bits(coef), host_bits(pts.index_select(0, idx)),
+                             got, s)
+    print(p, rep)
+
+
+def test_dft_beyond_2g_elements():
+    n = 1 << 20
+    batch = G // n + 1                      # vector 2048 starts at element 2^31
+    gen = torch.Generator(device=gu.DEV).manual_seed(61)
+    x = torch.view_as_complex(torch.randn((batch, n, 2), generator=gen, device=gu.DEV))
+    guard = 1024
+    ybuf = torch.full((batch * n + guard,), complex(7.0, -7.0), dtype=torch.complex64,
+                      device=gu.DEV)
+    y = ybuf[: batch * n]
+    work = torch.empty(batch * n, dtype=torch.complex64, device=gu.DEV)
+    tcu.tcu_set_unit(32)
+    tcu.tcu_dft(x, y, work, n, batch)
+    torch.cuda.synchronize()
+    assert bool((ybuf[batch * n:] == complex(7.0, -7.0)).all()), "wrote past y"
+    vecs = [0, G // n - 1, G // n]
+    xs = x[vecs].cpu().numpy()
+    got = y.view(batch, n)[vecs].cpu().numpy()
+    rep = compare.check_dft(xs, got, ref=oracle.dft(xs))
+    print(batch, n, rep)
+
+
+def test_tc_beyond_2g_bytes():
+    """Closure of a disjoint union of cycles on 2^16 vertices (X holds 2^32
+    bytes): every vertex reaches exactly the vertices of its own cycle."""
+    n = 1 << 16
+    src, dst, label = inputs.cycle_graph(n, max_len=6000, seed=71)
+    rows_total = n * n
+    buf = torch.full((rows_total + 4096,), 0x5A, dtype=torch.uint8, device=gu.DEV)
+    X = buf[:rows_total].view(n, n)
+    X.zero_()
+    X[src.to(gu.DEV), dst.to(gu.DEV)] = 1
+    tcu.tcu_set_unit(32)
+    tcu.tcu_transitive_closure(X, n, n)
+    torch.cuda.synchronize()
+    assert bool((buf[rows_total:] == 0x5A).all()), "wrote past X"
+    sizes = torch.bincount(label)
+    assert int(X.sum(dtype=torch.int64)) == int((sizes * sizes).sum())
+    rows = sample(n, G // n, seed=5, k=64)
+    got = X.index_select(0, torch.from_numpy(rows).to(gu.DEV)).cpu().numpy()
+    lab = label.numpy()
+    want = (lab[rows][:, None] == lab[None, :]).astype(np.uint8)
+    assert np.array_equal(got, want)

@@ -123,3 +123,20 @@ def _mutants(oracle_mod):
 def test_tc_pin_catches_planted_mistakes(oracle_mod):
     for mut in _mutants(oracle_mod):
         assert not bfs_pin(mut), mut.__name__
+
+
+@pytest.mark.parametrize("n,max_len,seed", [(1, 1, 0), (50, 1, 1), (300, 40, 2), (700, 700, 3)])
+def test_tc_union_of_cycles_closed_form(oracle_mod, n, max_len, seed):
+    """A disjoint union of directed cycles (runs of one vertex are self
+    loops): every vertex reaches exactly the vertices of its own cycle,
+    itself included.  The large-size GPU test checks against this form."""
+    from paper_1908_06649_amd import inputs
+    src, dst, label = inputs.cycle_graph(n, max_len, seed)
+    d = np.zeros((n, n), np.uint8)
+    d[src.numpy(), dst.numpy()] = 1
+    lab = label.numpy()
+    want = (lab[:, None] == lab[None, :]).astype(np.uint8)
+    assert np.array_equal(oracle_mod.transitive_closure(d), want)
+    if max_len > 3:                  # some cycle is longer than 3: paths of length > 2
+        one_squaring = _mutants(oracle_mod)[0]
+        assert not np.array_equal(one_squaring(d), want)
