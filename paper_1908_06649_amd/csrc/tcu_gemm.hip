@@ -347,11 +347,14 @@ __device__ __forceinline__ void vm_wait_barrier() {
   asm volatile("s_barrier" ::: "memory");
 }
 
-template <int DT, int kRing>
+// kEdge: C's edge may cut through tiles and K may end inside a stage (the
+// ragged shapes); without it every tile and stage is whole.
+template <int DT, int kRing, bool kEdge>
 __global__ __attribute__((amdgpu_flat_work_group_size(512, 512), amdgpu_waves_per_eu(2, 2))) void
 gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restrict__ B,
                unsigned char *__restrict__ C, int K, int64_t lda, int64_t ldb, int64_t ldc,
-               int accum, int tiles_m, int tiles_n, int nsplit, TileRemap remap) {
+               int accum, int tiles_m, int tiles_n, int nsplit, int m_lim, int n_lim,
+               TileRemap remap) {
   constexpr bool kI8 = (in_bytes(DT) == 1);
   constexpr int ES = in_bytes(DT);
   constexpr int OB = out_bytes(DT);
@@ -372,7 +375,11 @@ gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restr
   // partial tile into C atomically.
   const int tiles = tiles_m * tiles_n;
   const int total = tiles * nsplit;
-  const int nk_all = K / KE;
+  // Stages of the contracted index; when K is not a whole number of stages
+  // the last one holds k_tail < KE elements and is loaded element-wise with
+  // zeros past K (the zero padding of a ragged dimension).
+  const int nk_all = kEdge ? (K + KE - 1) / KE : K / KE;
+  const int k_tail = K - (nk_all - 1) * KE;
   const int64_t lda_b = lda * ES, ldb_b = ldb * ES, ldc_b = ldc * OB;
   const int lane = threadIdx.x & 63;
   const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -380,10 +387,42 @@ gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restr
   const int r = lane & 15, g = lane >> 4;
   int item = blockIdx.x;
   int m0, n0, nk;
+  int tail_t = -1;   // item-relative index of a partial last stage, if the item holds it
   // This wave's DMA share of a stage: group 0 -> A blocks 4q..4q+3 (16 rows
   // each, stored chunk-major), group 1 -> B blocks 4q..4q+3 (1 KiB each).
   // Wave-uniform 64-bit base + per-lane 32-bit offsets (saddr form).
   const unsigned char *gbase;
+  unsigned voff[kDma];
+  // Per-lane offsets.  In a tile that crosses the edge of C (rows >= m_lim
+  // or columns >= n_lim) a lane past the edge loads the last row of A, or
+  // the last 16-byte chunk of B's row, inside it instead: every load stays
+  // in the operands, every DMA instruction is issued (the wait counts rely
+  // on it), and the products it feeds are never stored.
+  auto set_voff = [&]() {
+#pragma unroll
+    for (int i = 0; i < kDma; ++i) {
+      const int blk = q * 4 + i;
+      if (grp == 0) {
+        int row = blk * 16 + (lane & 15);
+        if (kEdge && m0 + row >= m_lim) row = m_lim - 1 - m0;
+        voff[i] = (unsigned)(row * lda_b) + 16u * (lane >> 4);
+      } else {
+        int krow, c;
+        if constexpr (!kI8) {
+          krow = blk * 2 + (lane >> 5);
+          c = (lane & 31) ^ fb16_swz(krow);
+        } else {
+          krow = blk * 4 + (lane >> 4);
+          c = (lane & 15) ^ fb8_swz(krow);
+        }
+        if constexpr (kEdge) {
+          const int c_last = (n_lim - n0) * ES / 16 - 1;
+          if (c > c_last) c = c_last;
+        }
+        voff[i] = (unsigned)(krow * ldb_b) + 16u * c;
+      }
+    }
+  };
   auto place = [&](int w) {
     const int slice = w / tiles;
     int tm, tn;
@@ -392,31 +431,60 @@ gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restr
     n0 = remap.n_base + tn * 256 + (tn >= remap.band_n ? remap.skip_n : 0);
     const int s_begin = (int)((int64_t)nk_all * slice / nsplit);
     nk = (int)((int64_t)nk_all * (slice + 1) / nsplit) - s_begin;
+    if constexpr (kEdge) tail_t = (k_tail < KE && s_begin + nk == nk_all) ? nk - 1 : -1;
     gbase = grp == 0 ? A + (int64_t)m0 * lda_b + (int64_t)s_begin * kFastKB
                      : B + (int64_t)n0 * ES + (int64_t)s_begin * KE * ldb_b;
+    if constexpr (kEdge) set_voff();
   };
   place(item);
+  if constexpr (!kEdge) set_voff();    // the same for every tile
   const int64_t gstep = grp == 0 ? (int64_t)kFastKB : (int64_t)KE * ldb_b;
-  unsigned voff[kDma];
-#pragma unroll
-  for (int i = 0; i < kDma; ++i) {
-    const int blk = q * 4 + i;
-    if (grp == 0) {
-      voff[i] = (unsigned)((blk * 16 + (lane & 15)) * lda_b) + 16u * (lane >> 4);
-    } else {
-      int krow, c;
-      if constexpr (!kI8) {
-        krow = blk * 2 + (lane >> 5);
-        c = (lane & 31) ^ fb16_swz(krow);
-      } else {
-        krow = blk * 4 + (lane >> 4);
-        c = (lane & 15) ^ fb8_swz(krow);
-      }
-      voff[i] = (unsigned)(krow * ldb_b) + 16u * c;
-    }
-  }
   const unsigned lds0 = (grp == 0 ? lds_addr(sA) : lds_addr(sB)) + q * 4 * 1024;
+  // The partial last stage: the same 16 bytes per lane into the same LDS
+  // bytes as the DMA would write (lane L of instruction i at 1024 i + 16 L),
+  // read with ordinary loads that skip every element past K -- A's columns
+  // beyond K (the next row, or past the array) and B's rows beyond K -- and
+  // write zeros there.  A wave may take any number of these loads (none when
+  // its part lies wholly past K), so the issue ends by waiting for every
+  // load of the wave: afterwards no load of this or an older stage is in
+  // flight, and the stage waits below (which count kDma loads per later
+  // stage in flight) hold trivially until the next tile's stages.
+  auto issue_tail = [&](int slot_, int t) {
+    const unsigned char *base = gbase + (int64_t)t * gstep;
+    unsigned char *dst = (grp == 0 ? sA : sB) + q * 4 * 1024 + slot_ * kFastStage;
+#pragma unroll
+    for (int i = 0; i < kDma; ++i) {
+      const int blk = q * 4 + i;
+      u32x4 v = {0u, 0u, 0u, 0u};
+      const unsigned char *src = base + voff[i];
+      if (grp == 0) {
+        const int valid = k_tail - (lane >> 4) * (16 / ES);   // elements of this chunk in K
+        if (valid >= 16 / ES) {
+          v = *(const u32x4 *)src;
+        } else if (valid > 0) {
+          unsigned w[4] = {0u, 0u, 0u, 0u};
+          for (int e = 0; e < valid; ++e) {
+            const unsigned x = ES == 2 ? (unsigned)((const unsigned short *)src)[e]
+                                       : (unsigned)src[e];
+            w[(e * ES) >> 2] |= x << (8 * ((e * ES) & 3));
+          }
+          v = u32x4{w[0], w[1], w[2], w[3]};
+        }
+      } else {
+        const int krow = kI8 ? blk * 4 + (lane >> 4) : blk * 2 + (lane >> 5);
+        if (krow < k_tail) v = *(const u32x4 *)src;
+      }
+      *(u32x4 *)(dst + i * 1024 + 16 * lane) = v;
+    }
+    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
+  };
   auto issue = [&](int slot_, int t) {
+    if constexpr (kEdge) {
+      if (t == tail_t) {
+        issue_tail(slot_, t);
+        return;
+      }
+    }
     const unsigned char *base = gbase + (int64_t)t * gstep;
 #pragma unroll
     for (int i = 0; i < kDma; ++i) dma_lds16_saddr(base, voff[i], lds0 + slot_ * kFastStage + i * 1024);
@@ -569,6 +637,12 @@ gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restr
         const int col = n0 + q * 64 + fn * 16 + 4 * g;
         return C + (int64_t)row * ldc_b + (int64_t)col * OB;
       };
+      // The lane's 4 columns lie wholly inside or wholly outside C (n_lim is
+      // a multiple of 4).
+      auto in_c = [&](int fn, int fm) {
+        return !kEdge ||
+               (m0 + grp * 128 + fm * 16 + r < m_lim && n0 + q * 64 + fn * 16 + 4 * g < n_lim);
+      };
       constexpr bool kSplittable = DT == TCU_F16_F32 || DT == TCU_BF16_F32 || DT == TCU_I8_I32;
       if (kSplittable && nsplit > 1) {
         // Partial tiles: consecutive atomic adds go to different rows (and
@@ -577,7 +651,8 @@ gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restr
 #pragma unroll
           for (int fn = 0; fn < FN; ++fn)
 #pragma unroll
-            for (int fm = 0; fm < FM; ++fm) atomic_add_out4<DT>(out_ptr(fn, fm), acc[fn][fm]);
+            for (int fm = 0; fm < FM; ++fm)
+              if (in_c(fn, fm)) atomic_add_out4<DT>(out_ptr(fn, fm), acc[fn][fm]);
         }
       } else {
         // Blocks fn and fn + 1 hold the two 64-byte halves of 128-byte rows
@@ -588,7 +663,7 @@ gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restr
         for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
           for (int fn = 0; fn < FN; ++fn)
-            store_out4<DT, true>(out_ptr(fn, fm), acc[fn][fm], 4, accum != 0);
+            if (in_c(fn, fm)) store_out4<DT, true>(out_ptr(fn, fm), acc[fn][fm], 4, accum != 0);
       }
     }
     // Every wave finished reading the ring at the last barrier of the loop.
@@ -799,6 +874,39 @@ GemmPath gemm_path() {
   return GemmPath::kAuto;
 }
 
+// The general and small-tile kernels: the product on shapes the full-tile
+// kernel does not take.
+template <int DT>
+hipError_t launch_general(const RectArgs &a, GemmPath path, bool vec, hipStream_t stream,
+                          int num_cus) {
+  constexpr int ES = in_bytes(DT);
+  const int64_t big_tiles = ((a.M + 255) / 256) * ((a.N + 255) / 256);
+  // Element-wise operand access (pitches not multiples of 16 bytes).
+  if (!vec) return launch_cfg<DT, 64, 64, 2, 2, false>(a, stream);
+  const int64_t mid_tiles = ((a.M + 127) / 128) * ((a.N + 127) / 128);
+  // The small-tile ring kernel: 16-bit inputs, whole 64 x 64 tiles and
+  // 128-byte K stages, where the general kernel would take 64 x 64 tiles
+  // (or where forced, TCU_GEMM_KERNEL=ring).
+  if constexpr (ES == 2) {
+    const bool ring_ok = path != GemmPath::kGeneral && path != GemmPath::kFast &&
+                         a.M % 64 == 0 && a.N % 64 == 0 && a.K % 64 == 0 && a.K > 0 &&
+                         16 * a.lda * ES < ((int64_t)1 << 32) &&
+                         16 * a.ldb * ES < ((int64_t)1 << 32);
+    if (ring_ok && (path == GemmPath::kRing || mid_tiles < num_cus)) {
+      const int tm = (int)(a.M / 64), tn = (int)(a.N / 64);
+      hipLaunchKernelGGL((gemm_ring_kernel<DT, 8>), dim3(tm * tn), dim3(256), 0, stream,
+                         (const unsigned char *)a.A, (const unsigned char *)a.B,
+                         (unsigned char *)a.C, (int)a.K, a.lda, a.ldb, a.ldc, a.accum ? 1 : 0,
+                         tm, tn);
+      return hipGetLastError();
+    }
+  }
+  // Otherwise the largest tiles that still give every CU a workgroup.
+  if (big_tiles >= num_cus) return launch_cfg<DT, 256, 256, 2, 2, true>(a, stream);
+  if (mid_tiles >= num_cus) return launch_cfg<DT, 128, 128, 2, 2, true>(a, stream);
+  return launch_cfg<DT, 64, 64, 2, 2, true>(a, stream);
+}
+
 template <int DT>
 hipError_t launch_dt(const RectArgs &a, hipStream_t stream, int num_cus) {
   constexpr int ES = in_bytes(DT), OB = out_bytes(DT);
@@ -846,36 +954,59 @@ hipError_t launch_dt(const RectArgs &a, hipStream_t stream, int num_cus) {
     const int want = gv && std::atoi(gv) > 0 ? std::atoi(gv) : num_cus;
     const int items = tm * tn * nsplit;
     const int grid = want < items ? want : items;
-    hipLaunchKernelGGL((gemm_pp_kernel<DT, TCU_RING>), dim3(grid), dim3(512), 0, stream,
+    hipLaunchKernelGGL((gemm_pp_kernel<DT, TCU_RING, false>), dim3(grid), dim3(512), 0, stream,
                        (const unsigned char *)a.A, (const unsigned char *)a.B,
                        (unsigned char *)a.C, (int)a.K, a.lda, a.ldb, a.ldc, a.accum ? 1 : 0,
-                       tm, tn, nsplit, TileRemap{});
+                       tm, tn, nsplit, (int)a.M, (int)a.N, TileRemap{});
     return hipGetLastError();
   }
-  // Element-wise operand access (pitches not multiples of 16 bytes).
-  if (!vec) return launch_cfg<DT, 64, 64, 2, 2, false>(a, stream);
-  const int64_t mid_tiles = ((a.M + 127) / 128) * ((a.N + 127) / 128);
-  // The small-tile ring kernel: 16-bit inputs, whole 64 x 64 tiles and
-  // 128-byte K stages, where the general kernel would take 64 x 64 tiles
-  // (or where forced, TCU_GEMM_KERNEL=ring).
-  if constexpr (ES == 2) {
-    const bool ring_ok = path != GemmPath::kGeneral && path != GemmPath::kFast &&
-                         a.M % 64 == 0 && a.N % 64 == 0 && a.K % 64 == 0 && a.K > 0 &&
-                         16 * a.lda * ES < ((int64_t)1 << 32) &&
-                         16 * a.ldb * ES < ((int64_t)1 << 32);
-    if (ring_ok && (path == GemmPath::kRing || mid_tiles < num_cus)) {
-      const int tm = (int)(a.M / 64), tn = (int)(a.N / 64);
-      hipLaunchKernelGGL((gemm_ring_kernel<DT, 8>), dim3(tm * tn), dim3(256), 0, stream,
-                         (const unsigned char *)a.A, (const unsigned char *)a.B,
-                         (unsigned char *)a.C, (int)a.K, a.lda, a.ldb, a.ldc, a.accum ? 1 : 0,
-                         tm, tn);
-      return hipGetLastError();
+  // Ragged shapes (dimensions that are not multiples of the tile or of a
+  // stage, zero-padded), large enough to give every CU a 256 x 256 tile:
+  //   * N a whole number of 16-byte chunks: the full-tile kernel alone, its
+  //     edge tiles loading clamped rows and chunks and storing only inside
+  //     C, the contracted index's partial last stage zero-padded;
+  //   * otherwise the full-tile kernel takes the 256-aligned interior --
+  //     rows [0, M0) and columns [0, N0) over the whole K -- and the
+  //     general kernel the bottom rows [M0, M) (all columns) and the right
+  //     columns [N0, N) of rows [0, M0).
+  // Every output element is formed by one launch over the whole K, so a
+  // bfloat16 output is still rounded once.
+  const int64_t M0 = a.M / 256 * 256, N0 = a.N / 256 * 256;
+  const bool edges_in_kernel = (a.N * ES) % 16 == 0;
+  const int64_t tm_all = edges_in_kernel ? (a.M + 255) / 256 : M0 / 256;
+  const int64_t tn_all = edges_in_kernel ? (a.N + 255) / 256 : N0 / 256;
+  const bool ragged_ok = path == GemmPath::kAuto && vec && a.K >= KE && tm_all >= 1 &&
+                         tn_all >= 1 && tm_all * tn_all >= num_cus &&
+                         256 * a.lda * ES < ((int64_t)1 << 32) &&
+                         KE * a.ldb * ES < ((int64_t)1 << 32);
+  if (ragged_ok) {
+    const int tm = (int)tm_all, tn = (int)tn_all;
+    const int grid = num_cus < tm * tn ? num_cus : tm * tn;
+    hipLaunchKernelGGL((gemm_pp_kernel<DT, TCU_RING, true>), dim3(grid), dim3(512), 0, stream,
+                       (const unsigned char *)a.A, (const unsigned char *)a.B,
+                       (unsigned char *)a.C, (int)a.K, a.lda, a.ldb, a.ldc, a.accum ? 1 : 0,
+                       tm, tn, 1, (int)a.M, (int)a.N, TileRemap{});
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || edges_in_kernel) return e;
+    if (a.M > M0) {
+      RectArgs b = a;
+      b.A = (const unsigned char *)a.A + M0 * a.lda * ES;
+      b.C = (unsigned char *)a.C + M0 * a.ldc * OB;
+      b.M = a.M - M0;
+      e = launch_general<DT>(b, path, vec, stream, num_cus);
+      if (e != hipSuccess) return e;
     }
+    if (a.N > N0) {
+      RectArgs r = a;
+      r.B = (const unsigned char *)a.B + N0 * ES;
+      r.C = (unsigned char *)a.C + N0 * OB;
+      r.M = M0;
+      r.N = a.N - N0;
+      e = launch_general<DT>(r, path, vec, stream, num_cus);
+    }
+    return e;
   }
-  // Otherwise the largest tiles that still give every CU a workgroup.
-  if (big_tiles >= num_cus) return launch_cfg<DT, 256, 256, 2, 2, true>(a, stream);
-  if (mid_tiles >= num_cus) return launch_cfg<DT, 128, 128, 2, 2, true>(a, stream);
-  return launch_cfg<DT, 64, 64, 2, 2, true>(a, stream);
+  return launch_general<DT>(a, path, vec, stream, num_cus);
 }
 
 }  // namespace
@@ -914,7 +1045,7 @@ hipError_t launch_tc_rest(unsigned char *X, int64_t ld, int n, int k0, int Bk,
     TileRemap rm;
     rm.band_n = k0 / 256;
     rm.skip_n = 256;
-    return launch_tc_tiles(X, ld, k0, n / 256, n / 256 - 1, rm, stream, num_cus);
+    return launch_tc_tiles(X, ld, n, k0, n / 256, n / 256 - 1, rm, stream, num_cus);
   }
   if (ld % 16 == 0)
     return launch_bool<128, 128, true>(L, R, X, ld, n, n, Bk, k0, false, true, stream);
@@ -925,17 +1056,19 @@ bool tc_full_tiles(int64_t n, int Bk, int64_t ld) {
   return n % 256 == 0 && Bk == 256 && ld % 16 == 0 && 256 * ld < ((int64_t)1 << 32);
 }
 
-hipError_t launch_tc_tiles(unsigned char *X, int64_t ld, int k0, int tiles_m, int tiles_n,
-                           const TileRemap &remap, hipStream_t stream, int num_cus) {
+hipError_t launch_tc_tiles(unsigned char *X, int64_t ld, int n, int k0, int tiles_m,
+                           int tiles_n, const TileRemap &remap, hipStream_t stream,
+                           int num_cus) {
   // The D formula X[I, J] |= X[I, band] X[band, J] (band = [k0, k0 + 256))
   // on a tiles_m x tiles_n grid of 256 x 256 tiles placed by remap, by at
   // most num_cus persistent workgroups.
   const int items = tiles_m * tiles_n;
   if (items <= 0) return hipSuccess;
   const int grid = num_cus < items ? num_cus : items;
-  hipLaunchKernelGGL((gemm_pp_kernel<TCU_I8_BOOL, TCU_RING>), dim3(grid), dim3(512), 0, stream,
+  hipLaunchKernelGGL((gemm_pp_kernel<TCU_I8_BOOL, TCU_RING, false>), dim3(grid), dim3(512), 0,
+                     stream,
                      X + k0, X + (int64_t)k0 * ld, X, 256, ld, ld, ld, 1, tiles_m, tiles_n, 1,
-                     remap);
+                     n, n, remap);
   return hipGetLastError();
 }
 

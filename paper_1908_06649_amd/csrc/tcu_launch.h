@@ -51,8 +51,9 @@ hipError_t launch_tc_rest(unsigned char *X, int64_t ld, int n, int k0, int Bk,
 // Whether the full-tile kernel takes the D updates (n a multiple of 256,
 // whole bands, 16-byte row pitch), and its launch on a remapped tile grid.
 bool tc_full_tiles(int64_t n, int Bk, int64_t ld);
-hipError_t launch_tc_tiles(unsigned char *X, int64_t ld, int k0, int tiles_m, int tiles_n,
-                           const TileRemap &remap, hipStream_t stream, int num_cus);
+hipError_t launch_tc_tiles(unsigned char *X, int64_t ld, int n, int k0, int tiles_m,
+                           int tiles_n, const TileRemap &remap, hipStream_t stream,
+                           int num_cus);
 
 // Forward DFT of `batch` complex64 vectors of length n (a power of two):
 // ceil(log_s n) Cooley-Tukey levels alternating between work and y, the last

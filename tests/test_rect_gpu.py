@@ -98,6 +98,34 @@ def test_rect_ring_kernel(M, K, N, din, out, accumulate, pitch, monkeypatch):
     run_and_check(M, K, N, din, out, s, pitch, accumulate, seed=M + 5 * K + 11 * N)
 
 
+# Large ragged shapes (at least one 256 x 256 tile per CU): the full-tile
+# kernel with the contracted index's partial last stage zero-padded in the
+# kernel, and either its own edge tiles (N a whole number of 16-byte chunks)
+# or the general kernel for the bottom rows and right columns.  All three
+# dimensions ragged with edges in the kernel (4176: also for int8) or in
+# strips (4173); edges in the kernel for 16-bit inputs and in strips for
+# int8 (4104); only K; only M; a K tail of one element with one ragged
+# column (int8: K below one stage, the general kernel alone).
+LARGE_RAGGED = [(4101, 1000, 4176), (4101, 1000, 4173), (4375, 1000, 4104), (4096, 1000, 4096),
+                (4100, 1024, 4096), (4096, 33, 4097)]
+
+
+@pytest.mark.parametrize("accumulate", [False, True])
+@pytest.mark.parametrize("din,out", PAIRS)
+@pytest.mark.parametrize("M,K,N", LARGE_RAGGED)
+def test_rect_large_ragged_interior_and_edges(M, K, N, din, out, accumulate):
+    s = 32 if din == "bf16" else 16
+    run_and_check(M, K, N, din, out, s, "contiguous", accumulate, seed=M + K + N)
+
+
+@pytest.mark.parametrize("N", [4176, 4173])
+@pytest.mark.parametrize("accumulate", [False, True])
+@pytest.mark.parametrize("din,out", PAIRS)
+def test_rect_large_ragged_padded_pitches(din, out, accumulate, N):
+    s = 32 if din == "bf16" else 16
+    run_and_check(4101, 1000, N, din, out, s, "padded", accumulate, seed=77 + N)
+
+
 @pytest.mark.parametrize("din,out", PAIRS)
 @pytest.mark.parametrize("accumulate", [False, True])
 def test_rect_full_tiles_many_per_workgroup(din, out, accumulate, monkeypatch):
