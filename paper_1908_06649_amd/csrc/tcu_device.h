@@ -173,14 +173,19 @@ __device__ __forceinline__ u32x4 load_chunk(const unsigned char *p, int valid) {
 template <int DT, bool kVec, typename Acc>
 __device__ __forceinline__ void store_out4(unsigned char *p, Acc v, int valid, bool acc) {
   if constexpr (DT == TCU_I8_BOOL) {
-    // 0/1 output: old OR (sum > 0); the accumulate flag is implied.
+    // 0/1 output: old OR (sum > 0); the accumulate flag is implied.  OR is
+    // idempotent, so with no new flag nothing is read or written, and an
+    // unchanged word is not written back.
     if (kVec && valid >= 4) {
-      const unsigned old = *(const unsigned *)p;
-      unsigned w = 0;
+      unsigned f = 0;
 #pragma unroll
-      for (int e = 0; e < 4; ++e)
-        w |= (unsigned)((((old >> (8 * e)) & 0xffu) != 0u) | (v[e] > 0)) << (8 * e);
-      *(unsigned *)p = w;
+      for (int e = 0; e < 4; ++e) f |= (unsigned)(v[e] > 0) << (8 * e);
+      if (f == 0u) return;
+      const unsigned old = *(const unsigned *)p;
+      unsigned w = f;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) w |= (unsigned)(((old >> (8 * e)) & 0xffu) != 0u) << (8 * e);
+      if (w != old) *(unsigned *)p = w;
     } else {
 #pragma unroll
       for (int e = 0; e < 4; ++e)

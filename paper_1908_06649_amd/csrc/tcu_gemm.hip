@@ -616,18 +616,32 @@ gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restr
         }
       }
       __syncthreads();
+      // OR is idempotent: a chunk with no new flag is neither read nor
+      // written, and a chunk whose OR changes nothing is not written back
+      // (once the closure fills in, most of a band's update is such a no-op).
+      // The flags are read first so that all of a thread's C loads are in
+      // flight together.
       constexpr int kChunks = 256 * 16 / 512;   // 16-byte chunks per thread
-      u32x4 old[kChunks];
+      u32x4 f[kChunks], old[kChunks];
 #pragma unroll
       for (int j = 0; j < kChunks; ++j) {
         const int c = threadIdx.x + 512 * j, row = c >> 4, cc = c & 15;
-        old[j] = *(const u32x4 *)(C + (int64_t)(m0 + row) * ldc_b + n0 + 16 * cc);
+        f[j] = *(const u32x4 *)(stage + row * kStride + 16 * cc);
       }
 #pragma unroll
       for (int j = 0; j < kChunks; ++j) {
         const int c = threadIdx.x + 512 * j, row = c >> 4, cc = c & 15;
-        const u32x4 f = *(const u32x4 *)(stage + row * kStride + 16 * cc);
-        *(u32x4 *)(C + (int64_t)(m0 + row) * ldc_b + n0 + 16 * cc) = old[j] | f;
+        old[j] = u32x4{0u, 0u, 0u, 0u};
+        if ((f[j][0] | f[j][1] | f[j][2] | f[j][3]) != 0u)
+          old[j] = *(const u32x4 *)(C + (int64_t)(m0 + row) * ldc_b + n0 + 16 * cc);
+      }
+#pragma unroll
+      for (int j = 0; j < kChunks; ++j) {
+        const int c = threadIdx.x + 512 * j, row = c >> 4, cc = c & 15;
+        const u32x4 nw = old[j] | f[j];
+        const u32x4 d = nw ^ old[j];
+        if ((d[0] | d[1] | d[2] | d[3]) != 0u)
+          *(u32x4 *)(C + (int64_t)(m0 + row) * ldc_b + n0 + 16 * cc) = nw;
       }
       __syncthreads();   // staging reads done before the ring is refilled
     } else {
