@@ -3,6 +3,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <type_traits>
 #include <stdint.h>
 
 #include "tcu.h"
@@ -241,6 +242,35 @@ __device__ __forceinline__ void store_out4(unsigned char *p, Acc v, int valid, b
         }
       }
     }
+  }
+}
+
+// The accumulating store in two steps, for 4 values of one row that lie
+// inside the matrix at an aligned p: load_old4 reads the stored values'
+// bits and store_sum4 adds the new values to them and stores the result
+// (binary32 or int32 sum, one rounding to the output type), so that a wave
+// can have the loads of several blocks in flight before the first sum.
+template <int DT>
+using Old4 = typename std::conditional<DT == TCU_BF16_BF16, u32x2, u32x4>::type;
+
+template <int DT>
+__device__ __forceinline__ Old4<DT> load_old4(const unsigned char *p) {
+  return *(const Old4<DT> *)p;
+}
+
+template <int DT, typename Acc>
+__device__ __forceinline__ void store_sum4(unsigned char *p, Acc v, Old4<DT> o) {
+  static_assert(DT != TCU_I8_BOOL, "0/1 outputs are OR-ed, not added");
+  if constexpr (DT == TCU_BF16_BF16) {
+    v[0] += bf16_to_f32(o[0] & 0xffffu);
+    v[1] += bf16_to_f32(o[0] >> 16);
+    v[2] += bf16_to_f32(o[1] & 0xffffu);
+    v[3] += bf16_to_f32(o[1] >> 16);
+    *(u32x2 *)p = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+  } else if constexpr (DT == TCU_I8_I32) {
+    *(u32x4 *)p = bitcast<u32x4>(v) + o;
+  } else {
+    *(u32x4 *)p = bitcast<u32x4>(bitcast<f32x4>(v) + bitcast<f32x4>(o));
   }
 }
 

@@ -136,7 +136,7 @@ def test_rect_full_tiles_many_per_workgroup(din, out, accumulate, monkeypatch):
     run_and_check(768, 512, 1024, din, out, 32, "padded", accumulate, seed=12)
 
 
-@pytest.mark.parametrize("nsplit", [2, 3, 7])
+@pytest.mark.parametrize("nsplit", [2, 3, 4, 7])
 @pytest.mark.parametrize("din,out", PAIRS)
 @pytest.mark.parametrize("accumulate", [False, True])
 def test_rect_split_k(din, out, accumulate, nsplit, monkeypatch):
@@ -148,6 +148,18 @@ def test_rect_split_k(din, out, accumulate, nsplit, monkeypatch):
     monkeypatch.setenv("TCU_SPLIT_K", str(nsplit))
     run_and_check(512, 1344 if din != "i8" else 2688, 256, din, out, 32, "padded", accumulate,
                   seed=40 + nsplit)
+
+
+@pytest.mark.parametrize("din,out", PAIRS)
+def test_rect_split_k_many_items_per_workgroup(din, out, monkeypatch):
+    """Split-K items walked by a persistent grid of 5 workgroups: 6 tiles
+    x 3 K ranges = 18 items, the first 16 in the permuted (XCD-grouped)
+    order and the last 2 in their own."""
+    monkeypatch.setenv("TCU_GEMM_KERNEL", "fast")
+    monkeypatch.setenv("TCU_PP_GRID", "5")
+    monkeypatch.setenv("TCU_SPLIT_K", "3")
+    run_and_check(512, 768 if din != "i8" else 1536, 768, din, out, 32, "padded", True,
+                  seed=61)
 
 
 @pytest.mark.parametrize("s", [16, 32])
