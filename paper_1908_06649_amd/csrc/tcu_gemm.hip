@@ -353,8 +353,8 @@ template <int DT, int kRing, bool kEdge>
 __global__ __attribute__((amdgpu_flat_work_group_size(512, 512), amdgpu_waves_per_eu(2, 2))) void
 gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restrict__ B,
                unsigned char *__restrict__ C, int K, int64_t lda, int64_t ldb, int64_t ldc,
-               int accum, int tiles_m, int tiles_n, int nsplit, int m_lim, int n_lim,
-               TileRemap remap) {
+               int accum, int tiles_m, int tiles_n, int full, int nsplit, int m_lim,
+               int n_lim, TileRemap remap) {
   constexpr bool kI8 = (in_bytes(DT) == 1);
   constexpr int ES = in_bytes(DT);
   constexpr int OB = out_bytes(DT);
@@ -368,13 +368,16 @@ gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restr
   __shared__ __attribute__((aligned(1024))) unsigned char sA[kRing * kFastStage];
   __shared__ __attribute__((aligned(1024))) unsigned char sB[kRing * kFastStage];
 
-  // Work items: (K slice, output tile) pairs, slice-major so that the
-  // workgroups running at one time share the K range of their A and B
-  // panels.  With nsplit > 1 each item sums one contiguous range of whole
-  // stages (about nk_all / nsplit strips A_i of the unit) and adds its
-  // partial tile into C atomically.
+  // Work items: the first `full` tiles (in map_tile order) whole, then the
+  // other tiles as (K slice, tile) pairs, slice-major so that the workgroups
+  // running at one time share the K range of their A and B panels.  With
+  // nsplit > 1 such an item sums one contiguous range of whole stages
+  // (about nk_all / nsplit strips A_i of the unit) and adds its partial
+  // tile into C atomically.  full = 0 splits every tile; full = tiles (or
+  // nsplit = 1) none.
   const int tiles = tiles_m * tiles_n;
-  const int total = tiles * nsplit;
+  const int tail_tiles = tiles - full;
+  const int total = full + tail_tiles * nsplit;
   // Stages of the contracted index; when K is not a whole number of stages
   // the last one holds k_tail < KE elements and is loaded element-wise with
   // zeros past K (the zero padding of a ragged dimension).
@@ -423,22 +426,30 @@ gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restr
       }
     }
   };
-  // With split-K the items are few and long, and consecutive workgroup ids
-  // go round-robin to the 8 XCDs: item ids are permuted so that each XCD
+  // Split items are few and long, and consecutive workgroup ids go
+  // round-robin to the 8 XCDs: their ids are permuted so that each XCD
   // holds a contiguous run of them (one K range, a compact block of tiles),
   // and its concurrent workgroups share their A and B panels in its own L2
   // (measured: 2048 x 65536 x 2048 int8, split 4, 0.261 -> 0.235 ms).  The
   // items past the last multiple of 8 keep their ids.
-  const int xcd_body = nsplit > 1 ? total - total % 8 : 0;
+  const int split_items = nsplit > 1 ? total - full : 0;
+  const int xcd_body = split_items - split_items % 8;
+  bool split_item = false;   // the current item is a K slice (atomic epilogue)
   auto place = [&](int w) {
-    if (w < xcd_body) w = (w % 8) * (xcd_body / 8) + w / 8;
-    const int slice = w / tiles;
+    int pid = w, slice = 0;
+    split_item = nsplit > 1 && w >= full;
+    if (split_item) {
+      int v = w - full;
+      if (v < xcd_body) v = (v % 8) * (xcd_body / 8) + v / 8;
+      slice = v / tail_tiles;
+      pid = full + (v - slice * tail_tiles);
+    }
     int tm, tn;
-    map_tile(w - slice * tiles, tiles_m, tiles_n, tm, tn);
+    map_tile(pid, tiles_m, tiles_n, tm, tn);
     m0 = remap.m_base + tm * 256 + (tm >= remap.band_m ? remap.skip_m : 0);
     n0 = remap.n_base + tn * 256 + (tn >= remap.band_n ? remap.skip_n : 0);
-    const int s_begin = (int)((int64_t)nk_all * slice / nsplit);
-    nk = (int)((int64_t)nk_all * (slice + 1) / nsplit) - s_begin;
+    const int s_begin = split_item ? (int)((int64_t)nk_all * slice / nsplit) : 0;
+    nk = split_item ? (int)((int64_t)nk_all * (slice + 1) / nsplit) - s_begin : nk_all;
     if constexpr (kEdge) tail_t = (k_tail < KE && s_begin + nk == nk_all) ? nk - 1 : -1;
     gbase = grp == 0 ? A + (int64_t)m0 * lda_b + (int64_t)s_begin * kFastKB
                      : B + (int64_t)n0 * ES + (int64_t)s_begin * KE * ldb_b;
@@ -666,7 +677,7 @@ gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restr
                (m0 + grp * 128 + fm * 16 + r < m_lim && n0 + q * 64 + fn * 16 + 4 * g < n_lim);
       };
       constexpr bool kSplittable = DT == TCU_F16_F32 || DT == TCU_BF16_F32 || DT == TCU_I8_I32;
-      if (kSplittable && nsplit > 1) {
+      if (kSplittable && split_item) {
         // Partial tiles are added into C atomically.  In the accumulator
         // layout one atomic instruction would touch one element in each of
         // 16 rows, so every 64-byte line gets four separate requests; the
@@ -901,6 +912,62 @@ __global__ __launch_bounds__(256) void zero_fill_kernel(unsigned char *__restric
   }
 }
 
+// Zero the output tiles pid in [first, first + count) of a tiles_m x
+// tiles_n grid of 256 x 256 tiles of 4-byte values (placed by map_tile),
+// clipped to rows < m_lim and to the first row_bytes bytes of each row (a
+// multiple of 16): the starting value of the split tail tiles of a product
+// that overwrites C.
+__global__ __launch_bounds__(256) void zero_tiles_kernel(unsigned char *__restrict__ C,
+                                                         int64_t ldc_b, int tiles_m, int tiles_n,
+                                                         int first, int count, int m_lim,
+                                                         int64_t row_bytes) {
+  constexpr int kChunks = 256 * 4 / 16;   // 16-byte chunks per tile row
+  const int64_t total = (int64_t)count * 256 * kChunks;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int t = (int)(i / (256 * kChunks));
+    const int rem = (int)(i - (int64_t)t * 256 * kChunks);
+    int tm, tn;
+    map_tile(first + t, tiles_m, tiles_n, tm, tn);
+    const int row = tm * 256 + rem / kChunks;
+    const int64_t cb = (int64_t)tn * 1024 + 16 * (rem % kChunks);
+    if (row < m_lim && cb < row_bytes)
+      *(u32x4 *)(C + (int64_t)row * ldc_b + cb) = u32x4{0u, 0u, 0u, 0u};
+  }
+}
+
+// The tail split: when a persistent grid of `grid` workgroups walks `tiles`
+// whole tiles and the last round holds only tiles % grid of them, most CUs
+// would idle through it.  Those tail tiles are cut into nsplit K ranges
+// instead (at least kMinStages stages each, at most grid / tail of them),
+// added into C atomically, so the last round is about 1 / nsplit as long.
+// binary32 and int32 outputs only (a bfloat16 output is rounded once from
+// the whole sum).  TCU_TAIL_SPLIT=<n> forces n ranges (tests).  Returns
+// nsplit (1: no tail split) and sets *full to the number of whole tiles.
+template <int DT>
+int tail_split(int tiles, int grid, int64_t stages, int kMinStages, int *full) {
+  *full = tiles;
+  if (DT == TCU_BF16_BF16 || tiles <= grid || tiles % grid == 0) return 1;
+  const int tail = tiles % grid;
+  int64_t ns = grid / tail;
+  const int64_t cap = stages / kMinStages;
+  if (ns > cap) ns = cap;
+  const char *tv = std::getenv("TCU_TAIL_SPLIT");
+  if (tv && std::atoi(tv) > 0) ns = std::atoi(tv) < stages ? std::atoi(tv) : stages;
+  if (ns < 2) return 1;
+  *full = tiles - tail;
+  return (int)ns;
+}
+
+// Zero the tail tiles [full, tiles) of an overwriting product split by
+// tail_split (C of 4-byte values, row pitch ldc_b bytes).
+hipError_t zero_tail(unsigned char *C, int64_t ldc_b, int tm, int tn, int full, int m_lim,
+                     int64_t row_bytes, hipStream_t stream, int num_cus) {
+  hipLaunchKernelGGL(zero_tiles_kernel, dim3(num_cus * 4), dim3(256), 0, stream, C, ldc_b, tm,
+                     tn, full, tm * tn - full, m_lim, row_bytes);
+  return hipGetLastError();
+}
+
 template <int DT, int BM, int BN, int WM, int WN, bool kVec>
 hipError_t launch_cfg(const RectArgs &a, hipStream_t stream) {
   const int tiles_m = (int)((a.M + BM - 1) / BM), tiles_n = (int)((a.N + BN - 1) / BN);
@@ -1022,12 +1089,22 @@ hipError_t launch_dt(const RectArgs &a, hipStream_t stream, int num_cus) {
     // tiles).
     const char *gv = std::getenv("TCU_PP_GRID");
     const int want = gv && std::atoi(gv) > 0 ? std::atoi(gv) : num_cus;
-    const int items = tm * tn * nsplit;
+    int full = 0;
+    if (nsplit == 1) {
+      const int g0 = want < tm * tn ? want : tm * tn;
+      nsplit = tail_split<DT>(tm * tn, g0, a.K / KE, kMinSplitStages, &full);
+      if (nsplit > 1 && !a.accum) {
+        const hipError_t e = zero_tail((unsigned char *)a.C, a.ldc * OB, tm, tn, full,
+                                       (int)a.M, a.N * OB, stream, num_cus);
+        if (e != hipSuccess) return e;
+      }
+    }
+    const int items = full + (tm * tn - full) * nsplit;
     const int grid = want < items ? want : items;
     hipLaunchKernelGGL((gemm_pp_kernel<DT, TCU_RING, false>), dim3(grid), dim3(512), 0, stream,
                        (const unsigned char *)a.A, (const unsigned char *)a.B,
                        (unsigned char *)a.C, (int)a.K, a.lda, a.ldb, a.ldc, a.accum ? 1 : 0,
-                       tm, tn, nsplit, (int)a.M, (int)a.N, TileRemap{});
+                       tm, tn, full, nsplit, (int)a.M, (int)a.N, TileRemap{});
     return hipGetLastError();
   }
   // Ragged shapes (dimensions that are not multiples of the tile or of a
@@ -1052,10 +1129,20 @@ hipError_t launch_dt(const RectArgs &a, hipStream_t stream, int num_cus) {
   if (ragged_ok) {
     const int tm = (int)tm_all, tn = (int)tn_all;
     const int grid = num_cus < tm * tn ? num_cus : tm * tn;
+    // The tail tiles' zeroing is clipped to the kernel's part of C: all of
+    // it (N * OB is then a multiple of 16 bytes) or the 256-aligned interior.
+    int full = tm * tn;
+    const int nsplit = tail_split<DT>(tm * tn, grid, (a.K + KE - 1) / KE, kMinSplitStages, &full);
+    if (nsplit > 1 && !a.accum) {
+      hipError_t e = zero_tail((unsigned char *)a.C, a.ldc * OB, tm, tn, full,
+                               (int)(edges_in_kernel ? a.M : M0),
+                               (edges_in_kernel ? a.N : N0) * OB, stream, num_cus);
+      if (e != hipSuccess) return e;
+    }
     hipLaunchKernelGGL((gemm_pp_kernel<DT, TCU_RING, true>), dim3(grid), dim3(512), 0, stream,
                        (const unsigned char *)a.A, (const unsigned char *)a.B,
                        (unsigned char *)a.C, (int)a.K, a.lda, a.ldb, a.ldc, a.accum ? 1 : 0,
-                       tm, tn, 1, (int)a.M, (int)a.N, TileRemap{});
+                       tm, tn, full, nsplit, (int)a.M, (int)a.N, TileRemap{});
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || edges_in_kernel) return e;
     if (a.M > M0) {
@@ -1137,8 +1224,8 @@ hipError_t launch_tc_tiles(unsigned char *X, int64_t ld, int n, int k0, int tile
   const int grid = num_cus < items ? num_cus : items;
   hipLaunchKernelGGL((gemm_pp_kernel<TCU_I8_BOOL, TCU_RING, false>), dim3(grid), dim3(512), 0,
                      stream,
-                     X + k0, X + (int64_t)k0 * ld, X, 256, ld, ld, ld, 1, tiles_m, tiles_n, 1,
-                     n, n, remap);
+                     X + k0, X + (int64_t)k0 * ld, X, 256, ld, ld, ld, 1, tiles_m, tiles_n,
+                     tiles_m * tiles_n, 1, n, n, remap);
   return hipGetLastError();
 }
 

@@ -162,6 +162,44 @@ def test_rect_split_k_many_items_per_workgroup(din, out, monkeypatch):
                   seed=61)
 
 
+# The tail split: tiles beyond the last whole round of the persistent grid
+# cut into K ranges added atomically (binary32 and int32 outputs; C's tail
+# tiles zeroed first when overwriting).  (M, N, grid, forced ranges):
+# 10 tiles on 4 workgroups (2 tail tiles x 3 ranges, several rounds of split
+# items), 12 tiles on 8 (4 x 4 = 16 split items in the XCD-grouped order).
+@pytest.mark.parametrize("M,N,grid,ns", [(512, 1280, 4, 3), (768, 1024, 8, 4)])
+@pytest.mark.parametrize("din,out", PAIRS)
+@pytest.mark.parametrize("accumulate", [False, True])
+def test_rect_tail_split(M, N, grid, ns, din, out, accumulate, monkeypatch):
+    monkeypatch.setenv("TCU_GEMM_KERNEL", "fast")
+    monkeypatch.setenv("TCU_PP_GRID", str(grid))
+    monkeypatch.setenv("TCU_TAIL_SPLIT", str(ns))
+    K = 31 * 64 // ES[din]                  # 31 stages: uneven ranges
+    run_and_check(M, K, N, din, out, 32, "padded", accumulate, seed=M + N + ns)
+
+
+@pytest.mark.parametrize("din,out", PAIRS)
+def test_rect_tail_split_chosen_by_size(din, out, monkeypatch):
+    """Without forcing: 10 tiles on 4 workgroups and 64 stages give the 2
+    tail tiles 2 ranges of 32 stages."""
+    monkeypatch.setenv("TCU_GEMM_KERNEL", "fast")
+    monkeypatch.setenv("TCU_PP_GRID", "4")
+    run_and_check(512, 64 * 64 // ES[din], 1280, din, out, 32, "padded", False, seed=5)
+
+
+@pytest.mark.parametrize("accumulate", [False, True])
+@pytest.mark.parametrize("din,out", PAIRS)
+@pytest.mark.parametrize("M,K,N", [(4101, 1000, 4176), (4375, 1000, 4104)])
+def test_rect_large_ragged_tail_split(M, K, N, din, out, accumulate, monkeypatch):
+    """The ragged full-tile kernel with its tail tiles split 3 ways: edge
+    tiles in the kernel (17 x 17 tiles) and, for int8 on the second shape,
+    the 256-aligned interior (17 x 16 tiles) with the general kernel on the
+    strips."""
+    monkeypatch.setenv("TCU_TAIL_SPLIT", "3")
+    s = 32 if din == "bf16" else 16
+    run_and_check(M, K, N, din, out, s, "contiguous", accumulate, seed=M + K + N + 1)
+
+
 @pytest.mark.parametrize("s", [16, 32])
 @pytest.mark.parametrize("din,out", PAIRS)
 @pytest.mark.parametrize("M", [7, 16, 4099])
