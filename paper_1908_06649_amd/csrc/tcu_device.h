@@ -166,6 +166,22 @@ __device__ __forceinline__ u32x4 load_chunk(const unsigned char *p, int valid) {
   return v;
 }
 
+// One whole 16-byte chunk at p whose address is a multiple of kAl bytes (16,
+// 8 or 4): one vector load, or 2 / 4 naturally aligned narrower loads.
+template <int kAl>
+__device__ __forceinline__ u32x4 load16(const unsigned char *p) {
+  static_assert(kAl == 16 || kAl == 8 || kAl == 4, "chunk alignment 16, 8 or 4 bytes");
+  if constexpr (kAl == 16) {
+    return *(const u32x4 *)p;
+  } else if constexpr (kAl == 8) {
+    const u32x2 a = *(const u32x2 *)p, b = *(const u32x2 *)(p + 8);
+    return u32x4{a[0], a[1], b[0], b[1]};
+  } else {
+    const unsigned *q = (const unsigned *)p;
+    return u32x4{q[0], q[1], q[2], q[3]};
+  }
+}
+
 // Store 4 consecutive output values of one row of C at p (element col of
 // the row), of which the first `valid` (0..4) lie inside the matrix.  With
 // acc the stored values are read and added first (binary32 or int32 sum,

@@ -78,7 +78,10 @@ __device__ __forceinline__ void map_tile(int pid, int tiles_m, int tiles_n, int 
 // element by element with zeros in place of the missing elements, and only
 // in-range outputs are stored.  kVec: every pitch is a multiple of 16 bytes
 // (full chunks are vector loads, 4-value groups of C vector accesses).
-template <int DT, int BM, int BN, int WM, int WN, bool kVec>
+// Otherwise kAl > 0: A's and B's pitches are multiples of kAl (8 or 4) bytes,
+// and the whole chunks of interior tiles are loaded as 16 / kAl naturally
+// aligned pieces; kAl = 0: every chunk element by element.
+template <int DT, int BM, int BN, int WM, int WN, bool kVec, int kAl = 0>
 __global__ __attribute__((amdgpu_flat_work_group_size(64 * WM * WN, 64 * WM * WN),
                           amdgpu_waves_per_eu(1, 1))) void
 gemm_kernel(const unsigned char *__restrict__ A, const unsigned char *__restrict__ B,
@@ -131,13 +134,15 @@ gemm_kernel(const unsigned char *__restrict__ A, const unsigned char *__restrict
   // Whole tile inside M x N: only the last K-step can reach past K, and
   // only when K is not a multiple of the step.  Interior steps load whole
   // chunks with no per-element checks.
-  const bool interior = kVec && m0 + BM <= M && n0 + BN <= N;
+  constexpr int kLd = kVec ? 16 : kAl;         // alignment of whole-chunk loads
+  const bool inside = m0 + BM <= M && n0 + BN <= N;
+  const bool interior = kLd > 0 && inside;
   auto gload_full = [&](int k0) __attribute__((always_inline)) {
 #pragma unroll
     for (int i = 0; i < CA; ++i) {
       const int q = tid + NT * i;
       const int row = m0 + (q >> 3), kc = k0 + (q & 7) * EPC;
-      ra[i] = *(const u32x4 *)(A + (int64_t)row * lda_b + (int64_t)kc * ES);
+      ra[i] = load16<kLd ? kLd : 16>(A + (int64_t)row * lda_b + (int64_t)kc * ES);
     }
 #pragma unroll
     for (int i = 0; i < CB; ++i) {
@@ -148,7 +153,7 @@ gemm_kernel(const unsigned char *__restrict__ A, const unsigned char *__restrict
 #pragma unroll
       for (int rr = 0; rr < 8; ++rr) {
         const int k = k0 + 8 * kb + rr;
-        rb[i][rr] = *(const u32x4 *)(B + (int64_t)k * ldb_b + (int64_t)nc * ES);
+        rb[i][rr] = load16<kLd ? kLd : 16>(B + (int64_t)k * ldb_b + (int64_t)nc * ES);
       }
     }
   };
@@ -280,7 +285,7 @@ gemm_kernel(const unsigned char *__restrict__ A, const unsigned char *__restrict
       const int row = m0 + wm * WTM + 16 * fm + r;
       const int col = n0 + wn * WTN + 16 * fn + 4 * g;
       unsigned char *p = C + (int64_t)row * ldc_b + (int64_t)col * OB;
-      if (interior) {
+      if (kVec && inside) {
         store_out4<DT, true>(p, acc[fn][fm], 4, accum != 0);
       } else {
         const int valid = row < M ? min(max(N - col, 0), 4) : 0;
@@ -968,10 +973,10 @@ hipError_t zero_tail(unsigned char *C, int64_t ldc_b, int tm, int tn, int full, 
   return hipGetLastError();
 }
 
-template <int DT, int BM, int BN, int WM, int WN, bool kVec>
+template <int DT, int BM, int BN, int WM, int WN, bool kVec, int kAl = 0>
 hipError_t launch_cfg(const RectArgs &a, hipStream_t stream) {
   const int tiles_m = (int)((a.M + BM - 1) / BM), tiles_n = (int)((a.N + BN - 1) / BN);
-  hipLaunchKernelGGL((gemm_kernel<DT, BM, BN, WM, WN, kVec>), dim3(tiles_m * tiles_n),
+  hipLaunchKernelGGL((gemm_kernel<DT, BM, BN, WM, WN, kVec, kAl>), dim3(tiles_m * tiles_n),
                      dim3(64 * WM * WN), 0, stream, (const unsigned char *)a.A,
                      (const unsigned char *)a.B, (unsigned char *)a.C, (int)a.M, (int)a.N,
                      (int)a.K, a.lda, a.ldb, a.ldc, a.accum ? 1 : 0, tiles_m, tiles_n,
@@ -1018,9 +1023,23 @@ hipError_t launch_general(const RectArgs &a, GemmPath path, bool vec, hipStream_
                           int num_cus) {
   constexpr int ES = in_bytes(DT);
   const int64_t big_tiles = ((a.M + 255) / 256) * ((a.N + 255) / 256);
-  // Element-wise operand access (pitches not multiples of 16 bytes).
-  if (!vec) return launch_cfg<DT, 64, 64, 2, 2, false>(a, stream);
   const int64_t mid_tiles = ((a.M + 127) / 128) * ((a.N + 127) / 128);
+  // Pitches not all multiples of 16 bytes: whole chunks of A and B in 8- or
+  // 4-byte pieces where both pitches allow it, else element by element; C
+  // element by element.  128 x 128 tiles where they still give every CU a
+  // workgroup.
+  if (!vec) {
+    const int64_t pa = a.lda * ES, pb = a.ldb * ES;
+    const int al = pa % 8 == 0 && pb % 8 == 0 ? 8 : pa % 4 == 0 && pb % 4 == 0 ? 4 : 0;
+    if (mid_tiles >= num_cus) {
+      if (al == 8) return launch_cfg<DT, 128, 128, 2, 2, false, 8>(a, stream);
+      if (al == 4) return launch_cfg<DT, 128, 128, 2, 2, false, 4>(a, stream);
+      return launch_cfg<DT, 128, 128, 2, 2, false, 0>(a, stream);
+    }
+    if (al == 8) return launch_cfg<DT, 64, 64, 2, 2, false, 8>(a, stream);
+    if (al == 4) return launch_cfg<DT, 64, 64, 2, 2, false, 4>(a, stream);
+    return launch_cfg<DT, 64, 64, 2, 2, false, 0>(a, stream);
+  }
   // The small-tile ring kernel: 16-bit inputs, whole 64 x 64 tiles and
   // 128-byte K stages, where the general kernel would take 64 x 64 tiles
   // (or where forced, TCU_GEMM_KERNEL=ring).

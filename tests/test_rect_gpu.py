@@ -105,9 +105,13 @@ def test_rect_ring_kernel(M, K, N, din, out, accumulate, pitch, monkeypatch):
 # dimensions ragged with edges in the kernel (4176: also for int8) or in
 # strips (4173); edges in the kernel for 16-bit inputs and in strips for
 # int8 (4104); only K; only M; a K tail of one element with one ragged
-# column (int8: K below one stage, the general kernel alone).
+# column (int8: K below one stage, the general kernel alone).  Contiguous
+# pitches that are not multiples of 16 bytes take the general kernel with
+# 128 x 128 tiles, whole chunks loaded in 8-byte pieces (int8 K = 1000,
+# bfloat16 N = 4100), 4-byte pieces (int8 K = 1004) or element by element
+# (odd int8 or 16-bit pitches).
 LARGE_RAGGED = [(4101, 1000, 4176), (4101, 1000, 4173), (4375, 1000, 4104), (4096, 1000, 4096),
-                (4100, 1024, 4096), (4096, 33, 4097)]
+                (4100, 1024, 4096), (4096, 33, 4097), (4101, 1004, 4100)]
 
 
 @pytest.mark.parametrize("accumulate", [False, True])
