@@ -370,8 +370,14 @@ gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restr
   static_assert(kRing - 2 <= 3, "waits cover at most 3 later stages");
   typedef typename std::conditional<kI8, i32x4, f32x4>::type Acc;
 
-  __shared__ __attribute__((aligned(1024))) unsigned char sA[kRing * kFastStage];
-  __shared__ __attribute__((aligned(1024))) unsigned char sB[kRing * kFastStage];
+  // The ring (A and B parts), then, for 0/1 outputs, the epilogue's 256 x
+  // 256 flag tile in LDS of its own, so that the next tile's first stages
+  // can be loaded into the ring while the epilogue runs.
+  constexpr int kFlagBytes = DT == TCU_I8_BOOL ? 256 * 256 : 0;
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * kRing * kFastStage + kFlagBytes];
+  unsigned char *const sA = smem;
+  unsigned char *const sB = smem + kRing * kFastStage;
+  unsigned char *const sF = sB + kRing * kFastStage;
 
   // Work items: the first `full` tiles (in map_tile order) whole, then the
   // other tiles as (K slice, tile) pairs, slice-major so that the workgroups
@@ -618,15 +624,29 @@ gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restr
       }
     }
 
+    bool next_issued = false;   // the next tile's first stages are already in flight
     if constexpr (DT == TCU_I8_BOOL) {
       // 0/1 output (a quarter of the bytes of a binary32 tile): the flags
-      // (sum > 0) go through LDS -- the ring is free after the loop's last
-      // barrier -- so that the read-modify-write of C is done in whole
-      // 16-byte row chunks, consecutive threads on consecutive chunks.
-      // Row stride 272 bytes: the 16 rows one store instruction touches
-      // land in distinct banks.
-      constexpr int kStride = 272;
-      unsigned char *stage = sA;
+      // (sum > 0) go through LDS so that the read-modify-write of C is done
+      // in whole 16-byte row chunks, consecutive threads on consecutive
+      // chunks.  The flags have LDS of their own, so the next tile's first
+      // stages are issued first (the ring is free after the loop's last
+      // barrier) and load while this epilogue runs; the K loop is short here
+      // (one pivot band), so that latency would otherwise be paid per tile.
+      // Flag rows are 256 bytes with the 16-byte chunks XOR-swizzled by the
+      // row: the 16 rows one store instruction touches land in distinct
+      // banks, and a row's chunks are still one 256-byte row.
+      const int em0 = m0, en0 = n0;
+      if (item + (int)gridDim.x < total) {
+        item += gridDim.x;
+        place(item);
+        for (int s0 = 0; s0 < kRing; ++s0)
+          if (s0 < nk) issue(s0, s0);
+        next_issued = true;
+      }
+      auto flag_at = [&](int row, int byte) {
+        return sF + row * 256 + (((byte >> 4) ^ (row & 15)) << 4) + (byte & 15);
+      };
 #pragma unroll
       for (int fn = 0; fn < FN; ++fn) {
 #pragma unroll
@@ -636,7 +656,7 @@ gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restr
           unsigned w = 0;
 #pragma unroll
           for (int e = 0; e < 4; ++e) w |= (unsigned)(acc[fn][fm][e] > 0) << (8 * e);
-          *(unsigned *)(stage + row * kStride + col) = w;
+          *(unsigned *)flag_at(row, col) = w;
         }
       }
       __syncthreads();
@@ -650,14 +670,14 @@ gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restr
 #pragma unroll
       for (int j = 0; j < kChunks; ++j) {
         const int c = threadIdx.x + 512 * j, row = c >> 4, cc = c & 15;
-        f[j] = *(const u32x4 *)(stage + row * kStride + 16 * cc);
+        f[j] = *(const u32x4 *)flag_at(row, 16 * cc);
       }
 #pragma unroll
       for (int j = 0; j < kChunks; ++j) {
         const int c = threadIdx.x + 512 * j, row = c >> 4, cc = c & 15;
         old[j] = u32x4{0u, 0u, 0u, 0u};
         if ((f[j][0] | f[j][1] | f[j][2] | f[j][3]) != 0u)
-          old[j] = *(const u32x4 *)(C + (int64_t)(m0 + row) * ldc_b + n0 + 16 * cc);
+          old[j] = *(const u32x4 *)(C + (int64_t)(em0 + row) * ldc_b + en0 + 16 * cc);
       }
 #pragma unroll
       for (int j = 0; j < kChunks; ++j) {
@@ -665,9 +685,9 @@ gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restr
         const u32x4 nw = old[j] | f[j];
         const u32x4 d = nw ^ old[j];
         if ((d[0] | d[1] | d[2] | d[3]) != 0u)
-          *(u32x4 *)(C + (int64_t)(m0 + row) * ldc_b + n0 + 16 * cc) = nw;
+          *(u32x4 *)(C + (int64_t)(em0 + row) * ldc_b + en0 + 16 * cc) = nw;
       }
-      __syncthreads();   // staging reads done before the ring is refilled
+      __syncthreads();   // flag reads done before the next tile's epilogue rewrites them
     } else {
       // Epilogue: lane holds C[row][col .. col+3] of every accumulator block.
       auto out_ptr = [&](int fn, int fm) {
@@ -753,6 +773,7 @@ gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restr
       }
     }
     // Every wave finished reading the ring at the last barrier of the loop.
+    if (next_issued) continue;
     item += gridDim.x;
     if (item >= total) break;
     place(item);
@@ -1241,7 +1262,7 @@ hipError_t launch_tc_tiles(unsigned char *X, int64_t ld, int n, int k0, int tile
   const int items = tiles_m * tiles_n;
   if (items <= 0) return hipSuccess;
   const int grid = num_cus < items ? num_cus : items;
-  hipLaunchKernelGGL((gemm_pp_kernel<TCU_I8_BOOL, TCU_RING, false>), dim3(grid), dim3(512), 0,
+  hipLaunchKernelGGL((gemm_pp_kernel<TCU_I8_BOOL, 3, false>), dim3(grid), dim3(512), 0,
                      stream,
                      X + k0, X + (int64_t)k0 * ld, X, 256, ld, ld, ld, 1, tiles_m, tiles_n,
                      tiles_m * tiles_n, 1, n, n, remap);
