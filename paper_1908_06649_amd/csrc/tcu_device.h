@@ -167,18 +167,33 @@ __device__ __forceinline__ u32x4 load_chunk(const unsigned char *p, int valid) {
 }
 
 // One whole 16-byte chunk at p whose address is a multiple of kAl bytes (16,
-// 8 or 4): one vector load, or 2 / 4 naturally aligned narrower loads.
+// 8, 4, 2 or 1): one vector load, or 16 / kAl naturally aligned narrower
+// loads.
 template <int kAl>
 __device__ __forceinline__ u32x4 load16(const unsigned char *p) {
-  static_assert(kAl == 16 || kAl == 8 || kAl == 4, "chunk alignment 16, 8 or 4 bytes");
+  static_assert(kAl == 16 || kAl == 8 || kAl == 4 || kAl == 2 || kAl == 1,
+                "chunk alignment 16, 8, 4, 2 or 1 bytes");
   if constexpr (kAl == 16) {
     return *(const u32x4 *)p;
   } else if constexpr (kAl == 8) {
     const u32x2 a = *(const u32x2 *)p, b = *(const u32x2 *)(p + 8);
     return u32x4{a[0], a[1], b[0], b[1]};
-  } else {
+  } else if constexpr (kAl == 4) {
     const unsigned *q = (const unsigned *)p;
     return u32x4{q[0], q[1], q[2], q[3]};
+  } else if constexpr (kAl == 2) {
+    const unsigned short *q = (const unsigned short *)p;
+    u32x4 v;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[i] = (unsigned)q[2 * i] | ((unsigned)q[2 * i + 1] << 16);
+    return v;
+  } else {
+    u32x4 v;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      v[i] = (unsigned)p[4 * i] | ((unsigned)p[4 * i + 1] << 8) | ((unsigned)p[4 * i + 2] << 16) |
+             ((unsigned)p[4 * i + 3] << 24);
+    return v;
   }
 }
 

@@ -78,9 +78,9 @@ __device__ __forceinline__ void map_tile(int pid, int tiles_m, int tiles_n, int 
 // element by element with zeros in place of the missing elements, and only
 // in-range outputs are stored.  kVec: every pitch is a multiple of 16 bytes
 // (full chunks are vector loads, 4-value groups of C vector accesses).
-// Otherwise kAl > 0: A's and B's pitches are multiples of kAl (8 or 4) bytes,
-// and the whole chunks of interior tiles are loaded as 16 / kAl naturally
-// aligned pieces; kAl = 0: every chunk element by element.
+// Otherwise kAl > 0: A's and B's pitches are multiples of kAl (8, 4, 2 or 1)
+// bytes, and the whole chunks of interior tiles are loaded as 16 / kAl
+// naturally aligned pieces; kAl = 0: every chunk element by element.
 template <int DT, int BM, int BN, int WM, int WN, bool kVec, int kAl = 0>
 __global__ __attribute__((amdgpu_flat_work_group_size(64 * WM * WN, 64 * WM * WN),
                           amdgpu_waves_per_eu(1, 1))) void
@@ -1045,21 +1045,26 @@ hipError_t launch_general(const RectArgs &a, GemmPath path, bool vec, hipStream_
   constexpr int ES = in_bytes(DT);
   const int64_t big_tiles = ((a.M + 255) / 256) * ((a.N + 255) / 256);
   const int64_t mid_tiles = ((a.M + 127) / 128) * ((a.N + 127) / 128);
-  // Pitches not all multiples of 16 bytes: whole chunks of A and B in 8- or
-  // 4-byte pieces where both pitches allow it, else element by element; C
-  // element by element.  128 x 128 tiles where they still give every CU a
-  // workgroup.
+  // Pitches not all multiples of 16 bytes: whole chunks of A and B (interior
+  // tiles, full K steps) in the widest naturally aligned pieces both pitches
+  // allow (8, 4, 2 or 1 bytes), edges element by element; C element by
+  // element.  128 x 128 tiles where they still give every CU a workgroup.
   if (!vec) {
     const int64_t pa = a.lda * ES, pb = a.ldb * ES;
-    const int al = pa % 8 == 0 && pb % 8 == 0 ? 8 : pa % 4 == 0 && pb % 4 == 0 ? 4 : 0;
+    const int al = pa % 8 == 0 && pb % 8 == 0   ? 8
+                   : pa % 4 == 0 && pb % 4 == 0 ? 4
+                   : pa % 2 == 0 && pb % 2 == 0 ? 2
+                                                : 1;
     if (mid_tiles >= num_cus) {
       if (al == 8) return launch_cfg<DT, 128, 128, 2, 2, false, 8>(a, stream);
       if (al == 4) return launch_cfg<DT, 128, 128, 2, 2, false, 4>(a, stream);
-      return launch_cfg<DT, 128, 128, 2, 2, false, 0>(a, stream);
+      if (ES == 2 || al == 2) return launch_cfg<DT, 128, 128, 2, 2, false, 2>(a, stream);
+      return launch_cfg<DT, 128, 128, 2, 2, false, 1>(a, stream);
     }
     if (al == 8) return launch_cfg<DT, 64, 64, 2, 2, false, 8>(a, stream);
     if (al == 4) return launch_cfg<DT, 64, 64, 2, 2, false, 4>(a, stream);
-    return launch_cfg<DT, 64, 64, 2, 2, false, 0>(a, stream);
+    if (ES == 2 || al == 2) return launch_cfg<DT, 64, 64, 2, 2, false, 2>(a, stream);
+    return launch_cfg<DT, 64, 64, 2, 2, false, 1>(a, stream);
   }
   // The small-tile ring kernel: 16-bit inputs, whole 64 x 64 tiles and
   // 128-byte K stages, where the general kernel would take 64 x 64 tiles
