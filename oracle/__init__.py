@@ -21,9 +21,11 @@ numpy in/out:
   algorithm the section starts from (k outermost, then i, then j).
 * ``dft_direct(x)`` -- the DFT by its definition y = x^T W, W[r][c] =
   exp(-2 pi i r c / n) (Section 4.5), O(n^2) per vector, binary64;
-  ``dft(x)`` -- the same transform through numpy's binary64 FFT (a library
-  routine standing in for the definition at sizes where O(n^2) is too slow;
-  pinned against ``dft_direct``).
+  ``dft_direct_at(x, ks)`` -- the same definition at chosen output
+  frequencies only (O(n) each), which checks vectors of any length on a
+  sample of their outputs; ``dft(x)`` -- the whole transform through numpy's
+  binary64 FFT, an extra check at large sizes only (pinned against
+  ``dft_direct``).
 * ``mm_acc(A, B, C0, dtype, out)`` -- the accumulating form ``C0 + A*B``
   that the D functions of Sections 4.2 and 4.3 ask of the unit
   (X <- X + Y*Z); C0 holds stored output values ('f32', 'bf16' bits or
@@ -74,6 +76,8 @@ def _load():
     lib.oracle_transitive_closure.restype = ctypes.c_int
     lib.oracle_dft_direct.argtypes = [vp, i64, i64, vp]
     lib.oracle_dft_direct.restype = ctypes.c_int
+    lib.oracle_dft_direct_at.argtypes = [vp, i64, i64, vp, i64, vp]
+    lib.oracle_dft_direct_at.restype = ctypes.c_int
     lib.oracle_threads.argtypes = []
     lib.oracle_threads.restype = ctypes.c_int
     _lib = lib
@@ -207,6 +211,23 @@ def dft_direct(x: np.ndarray) -> np.ndarray:
     if rc != 0:
         raise ValueError("oracle rejected its arguments")
     return y.reshape(shape)
+
+
+def dft_direct_at(x: np.ndarray, ks) -> np.ndarray:
+    """The definition y[k] = sum_j x[j] exp(-2 pi i j k / n) at the output
+    frequencies ks only (binary64, O(n) per frequency), for every row of x
+    (complex, shape (batch, n) or (n,)); returns complex128 of shape
+    (batch, len(ks)) (or (len(ks),))."""
+    x = np.asarray(x, dtype=np.complex128)
+    one = x.ndim == 1
+    x2 = np.ascontiguousarray(x.reshape(-1, x.shape[-1]))
+    k = np.ascontiguousarray(ks, dtype=np.int64).ravel()
+    y = np.empty((x2.shape[0], k.size), dtype=np.complex128)
+    rc = _load().oracle_dft_direct_at(_ptr(x2.view(np.float64)), x2.shape[1], x2.shape[0],
+                                      _ptr(k), k.size, _ptr(y.view(np.float64)))
+    if rc != 0:
+        raise ValueError("oracle rejected its arguments")
+    return y[0] if one else y
 
 
 def dft(x: np.ndarray) -> np.ndarray:

@@ -184,26 +184,70 @@ def check_poly(dtype_in: str, dtype_out: str, coef_bits, pt_bits, got, s: int,
     return rep
 
 
-def check_dft(x: np.ndarray, got: np.ndarray, ref: np.ndarray | None = None) -> dict:
-    """Compare a GPU DFT (complex, rows = vectors) with the binary64 oracle:
-    relative Frobenius error <= 1e-3 per vector, and elementwise
-    |err_k| <= 1e-2 * sum_j |x_j| (the magnitude bound: |W| = 1).
-    ref: the oracle result when already computed."""
-    x = np.asarray(x, dtype=np.complex128).reshape(-1, np.asarray(x).shape[-1])
-    got = np.asarray(got, dtype=np.complex128).reshape(x.shape)
-    if ref is None:
-        from . import dft, dft_direct
-        ref = dft_direct(x) if x.shape[1] <= 1024 else dft(x)
-    ref = np.asarray(ref).reshape(x.shape)
+def dft_sample_freqs(n: int, seed: int = 0, k: int = 64) -> np.ndarray:
+    """Output frequencies a large transform is checked on against the
+    definition: 0, 1, 2, n/2 - 1, n/2, n/2 + 1, n - 2, n - 1 and k seeded
+    random ones (sorted, distinct, all of them when n is small)."""
+    if n <= k + 8:
+        return np.arange(n, dtype=np.int64)
+    fixed = np.array([0, 1, 2, n // 2 - 1, n // 2, n // 2 + 1, n - 2, n - 1], dtype=np.int64)
+    rng = np.random.default_rng(seed)
+    ks = set(fixed.tolist())
+    while len(ks) < k + fixed.size:
+        ks.add(int(rng.integers(0, n)))
+    return np.array(sorted(ks), dtype=np.int64)
+
+
+# Largest n whose whole transform the definition computes (O(n^2) per vector).
+DFT_FULL_MAX = 1024
+
+
+def _dft_report(got: np.ndarray, ref: np.ndarray, mag: np.ndarray) -> dict:
     err = np.abs(got - ref)
-    mag = np.sum(np.abs(x), axis=1, keepdims=True)
     den = np.linalg.norm(ref, axis=1)
     rel = np.where(den > 0, np.linalg.norm(got - ref, axis=1) / np.where(den > 0, den, 1), 0.0)
     with np.errstate(divide="ignore", invalid="ignore"):
         ratio = np.where(mag > 0, err / mag, np.where(err > 0, np.inf, 0.0))
-    rep = {"max_rel_frob": float(rel.max(initial=0.0)),
-           "max_err_over_l1": float(ratio.max(initial=0.0))}
-    assert np.all(np.isfinite(got)), rep
+    return {"max_rel_frob": float(rel.max(initial=0.0)),
+            "max_err_over_l1": float(ratio.max(initial=0.0))}
+
+
+def check_dft(x: np.ndarray, got: np.ndarray, ref: np.ndarray | None = None,
+              ks: np.ndarray | None = None, fft_extra: bool = True) -> dict:
+    """Compare a GPU DFT (complex, rows = vectors) with the binary64 oracle:
+    relative Frobenius error <= 1e-3 per vector, and elementwise
+    |err_k| <= 1e-2 * sum_j |x_j| (the magnitude bound: |W| = 1).
+
+    The reference is the definition y[k] = sum_j x[j] w^(jk): on every
+    output for n <= 1024, else on the frequencies ks (dft_sample_freqs(n)
+    when None; the relative Frobenius error is then taken over those
+    outputs).  For n > 1024 the whole transform is also compared with
+    numpy's binary64 FFT when fft_extra is set, an extra check only.
+    ref: the definition at ks (or everywhere) when already computed."""
+    from . import dft, dft_direct, dft_direct_at
+    x = np.asarray(x, dtype=np.complex128).reshape(-1, np.asarray(x).shape[-1])
+    got = np.asarray(got, dtype=np.complex128).reshape(x.shape)
+    n = x.shape[1]
+    assert np.all(np.isfinite(got)), "non-finite DFT output"
+    mag = np.sum(np.abs(x), axis=1, keepdims=True)
+    if ks is None and n > DFT_FULL_MAX:
+        ks = dft_sample_freqs(n)
+    if ks is None:
+        if ref is None:
+            ref = dft_direct(x)
+        rep = _dft_report(got, np.asarray(ref).reshape(x.shape), mag)
+        rep["freqs_checked"] = n
+    else:
+        ks = np.asarray(ks, dtype=np.int64)
+        if ref is None:
+            ref = dft_direct_at(x, ks)
+        rep = _dft_report(got[:, ks], np.asarray(ref).reshape(x.shape[0], ks.size), mag)
+        rep["freqs_checked"] = int(ks.size)
     assert rep["max_rel_frob"] <= REL_FROB, rep
     assert rep["max_err_over_l1"] <= ELEM, rep
+    if fft_extra and n > DFT_FULL_MAX:
+        extra = _dft_report(got, dft(x), mag)
+        rep["fft_max_rel_frob"] = extra["max_rel_frob"]
+        assert extra["max_rel_frob"] <= REL_FROB, rep
+        assert extra["max_err_over_l1"] <= ELEM, rep
     return rep

@@ -340,3 +340,38 @@ int oracle_dft_direct(const double *x, int64_t n, int64_t batch, double *y)
         }
     return 0;
 }
+
+/*
+ * The same definition of Section 4.5 at chosen output frequencies only:
+ * y[b][t] = sum_j x_b[j] exp(-2 pi i j k_t / n) for the nk frequencies
+ * k_t in ks (each 0 <= k_t < n), in binary64, the exponent j k_t reduced
+ * mod n exactly in integers as above.  O(n) per frequency, so vectors of
+ * any length can be checked on a sample of their outputs.
+ *   x: batch * n complex values (interleaved re, im doubles);
+ *   y: batch * nk complex values, row b holding the nk sampled outputs.
+ */
+int oracle_dft_direct_at(const double *x, int64_t n, int64_t batch, const int64_t *ks,
+                         int64_t nk, double *y)
+{
+    if (n < 1 || batch < 0 || nk < 0 || (nk > 0 && !ks)) return -1;
+    for (int64_t t = 0; t < nk; ++t)
+        if (ks[t] < 0 || ks[t] >= n) return -1;
+    const double two_pi = 6.283185307179586476925286766559;
+#pragma omp parallel for collapse(2) schedule(dynamic, 1)
+    for (int64_t b = 0; b < batch; ++b)
+        for (int64_t t = 0; t < nk; ++t) {
+            const double *xb = x + 2 * b * n;
+            const int64_t k = ks[t];
+            double re = 0.0, im = 0.0;
+            for (int64_t j = 0; j < n; ++j) {
+                const int64_t e = (int64_t)(((unsigned __int128)j * (unsigned __int128)k) % (unsigned __int128)n);
+                const double th = two_pi * (double)e / (double)n;
+                const double c = cos(th), s = sin(th);
+                re += xb[2 * j] * c + xb[2 * j + 1] * s;
+                im += xb[2 * j + 1] * c - xb[2 * j] * s;
+            }
+            y[2 * (b * nk + t)] = re;
+            y[2 * (b * nk + t) + 1] = im;
+        }
+    return 0;
+}

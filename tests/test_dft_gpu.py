@@ -1,12 +1,14 @@
 """GPU parity of the DFT (tcu_dft, Theorem 7, Section 4.5) against the CPU
-oracle (the definition for n <= 1024, numpy's binary64 FFT above), through
-the C ABI.  Bar: relative Frobenius error <= 1e-3 per vector and
-elementwise |err_k| <= 1e-2 * sum_j |x_j|."""
+oracle, through the C ABI: the definition y[k] = sum_j x[j] w^(jk) on every
+output for n <= 1024, and on at least 64 outputs of every vector above
+(k = 0, 1, 2, n/2 - 1, n/2, n/2 + 1, n - 2, n - 1 and 64 seeded random
+frequencies), with numpy's binary64 FFT of the whole transform as an extra
+check.  Bar: relative Frobenius error <= 1e-3 per vector and elementwise
+|err_k| <= 1e-2 * sum_j |x_j|."""
 import numpy as np
 import pytest
 import torch
 
-import oracle
 from oracle import compare
 from paper_1908_06649_amd import inputs, tcu
 
@@ -91,5 +93,6 @@ def test_dft_workload(name):
     sp = inputs.DFT_WORKLOADS[name]
     x = inputs.complex_signal(sp["batch"], sp["n"], sp["seed"])
     got = run_dft(x, sp["s"])
-    rep = compare.check_dft(x.numpy(), got, ref=oracle.dft(x.numpy()))
+    rep = compare.check_dft(x.numpy(), got)
+    assert rep["freqs_checked"] >= 64
     print(name, rep)

@@ -11,7 +11,6 @@ import numpy as np
 import pytest
 import torch
 
-import oracle
 from oracle import compare
 from paper_1908_06649_amd import inputs, tcu
 
@@ -118,7 +117,8 @@ def test_dft_beyond_2g_elements():
     vecs = [0, G // n - 1, G // n]
     xs = x[vecs].cpu().numpy()
     got = y.view(batch, n)[vecs].cpu().numpy()
-    rep = compare.check_dft(xs, got, ref=oracle.dft(xs))
+    rep = compare.check_dft(xs, got)          # the definition on >= 64 outputs per vector
+    assert rep["freqs_checked"] >= 64
     print(batch, n, rep)
 
 

@@ -7,7 +7,9 @@ complex exponential, a cosine, a shifted impulse), Parseval's identity,
 linearity, the circular shift theorem and the transform of the conjugate,
 and against exact rational arithmetic on sizes where the twiddles are exact
 (n = 1, 2, 4: W entries in {+-1, +-i}).  numpy's FFT (oracle.dft, used at
-large sizes) is checked against dft_direct.  Plausible mistakes (the
+large sizes) is checked against dft_direct.  dft_direct_at (the definition
+at chosen outputs, for vectors too long for the whole O(n^2) transform)
+equals dft_direct's entries and meets the closed forms at n = 2^16, 2^20.  Plausible mistakes (the
 conjugate sign, the transpose of a non-symmetric use, an off-by-one
 frequency) fail the pins.
 """
@@ -79,6 +81,63 @@ def test_fft_matches_definition(n):
     x = rand_c((3, n))
     d, f = oracle.dft_direct(x), oracle.dft(x)
     assert np.max(np.abs(d - f)) <= 1e-9 * np.sum(np.abs(x), axis=1).max()
+
+
+@pytest.mark.parametrize("n", [1, 3, 64, 100, 2048])
+def test_sampled_definition_equals_full(n):
+    """dft_direct_at is the definition at chosen outputs: equal to the whole
+    transform's entries (same binary64 evaluation order)."""
+    x = rand_c((3, n))
+    ks = np.unique(np.concatenate([[0, n // 2, n - 1], RNG.integers(0, n, 9)]))
+    assert np.array_equal(oracle.dft_direct_at(x, ks), oracle.dft_direct(x)[:, ks])
+    assert np.array_equal(oracle.dft_direct_at(x[0], ks), oracle.dft_direct(x[0])[ks])
+
+
+@pytest.mark.parametrize("n", [1 << 16, 1 << 20])
+def test_sampled_definition_closed_forms_large(n):
+    """At sizes where the whole definition is too slow, the sampled outputs
+    against closed forms: a shifted impulse delta[j - m] (y[k] = w^(mk),
+    exercising the exact reduction of m k mod n), and a pure exponential of
+    frequency f (y[k] = n at k = f, 0 elsewhere)."""
+    from oracle import compare
+    ks = compare.dft_sample_freqs(n, seed=5)
+    assert ks.size >= 72 and {0, 1, n // 2, n - 1} <= set(ks.tolist())
+    m = 12345
+    x = np.zeros(n, complex)
+    x[m] = 1
+    want = np.exp(-2j * np.pi * ((m * ks) % n) / n)
+    assert np.max(np.abs(oracle.dft_direct_at(x, ks) - want)) <= 1e-12
+    f = int(ks[len(ks) // 2])
+    e = np.exp(2j * np.pi * ((f * np.arange(n)) % n) / n)
+    want = np.where(ks == f, n, 0)
+    assert np.max(np.abs(oracle.dft_direct_at(e, ks) - want)) <= 1e-9 * n
+
+
+def test_sampled_definition_matches_fft_large():
+    """The sampled definition against numpy's FFT on random data, n = 2^14."""
+    from oracle import compare
+    n = 1 << 14
+    x = rand_c((2, n))
+    ks = compare.dft_sample_freqs(n, seed=7)
+    d = oracle.dft_direct_at(x, ks)
+    f = oracle.dft(x)[:, ks]
+    assert np.max(np.abs(d - f)) <= 1e-9 * np.sum(np.abs(x), axis=1).max()
+
+
+def test_check_dft_uses_definition_on_large_n():
+    """compare.check_dft takes the definition at >= 64 outputs for n > 1024
+    and rejects a transform that is wrong at only one of those outputs."""
+    from oracle import compare
+    n = 4096
+    x = rand_c((2, n))
+    y = oracle.dft(x)
+    rep = compare.check_dft(x, y)
+    assert rep["freqs_checked"] >= 72
+    ks = compare.dft_sample_freqs(n)
+    bad = y.copy()
+    bad[1, ks[40]] += 0.05 * np.sum(np.abs(x[1]))
+    with pytest.raises(AssertionError):
+        compare.check_dft(x, bad, fft_extra=False)
 
 
 def _mutants():
