@@ -12,10 +12,13 @@ JSON line:
   roofline   that kernel against the dense bf16 matrix-core peak, with the
              HBM traffic rocprofv3 counted for it (when still current)
   cpu_baseline  the CPU oracle timed on a bounded sample of the same product
-             on this host's cores, and the sampled rows' parity
+             on this host's cores (all rows when they fit ~15 s), and the
+             sampled rows' parity; "host" names the CPU model, nproc,
+             OMP_NUM_THREADS and the oracle's thread count
   secondary  the other workloads measured the same way: the very tall
              bf16 native call (GB/s vs HBM peak), the int8 product (TOP/s),
-             the 4096 x 16 native call and the N = 1024 fp16 product
+             the 4096 x 16 native call and the N = 1024 fp16 product, each
+             with its own cpu_baseline (oracle seconds and parity)
   poly       batch polynomial evaluation (tcu_poly_eval, Theorem 11) on 2^24
              points with 4096 coefficients: TFLOP/s of the method's 2pn
              multiply-adds vs the bf16 matrix-core peak
@@ -25,14 +28,19 @@ JSON line:
   tc         transitive closure (tcu_transitive_closure, Theorem 5) of a
              random 8192-vertex digraph: GB/s of the D updates' algorithmic
              traffic (each pivot band reads and writes the off-band n^2 bytes)
-             vs HBM peak, and boolean TOP/s (2 n^3 / t)
+             vs HBM peak, and boolean TOP/s (2 n^3 / t); every timed call
+             starts from the raw graph (restored outside the timed region);
+             the oracle's closure timed and compared exactly
   rect       the rectangular / accumulating product (tcu_gemm_rect):
              Corollary 1's sqrt(n) x r by r x sqrt(n) with r below and above
              sqrt(n), accumulating into C, and an order-8200 product that
              needs zero padding (TFLOP/s or TOP/s vs matrix-core peak)
   cost_model calls issued vs Theorem 2's count and bound, weak-model square
-             calls, model work, and the per-call latency l fitted as the
-             intercept of t(n) = a*n + l for native calls
+             calls, model work; the native call's cost t(n) = a*(n s) + l
+             fitted per type pair and unit size from a C timing loop; and per
+             configured workload the model time T = a*work + calls*l
+             (N^3/s + (N/s)^2 l for the product, n s + l for a native call)
+             against the measured time
 
 Timing: every measured call first runs back to back, untimed, for 0.3 s
 (the GPU leaves its idle clock state), then W untimed warmup calls, then K
@@ -159,10 +167,13 @@ class Workload:
             self.W = torch.empty_like(self.dA)
             return
         if self.spec["kind"] == "tc":
-            # the closure is computed in place; the algorithm's work does not
-            # depend on the data, so repeated calls on the same array time it
+            # The closure is computed in place, and its 0/1 epilogues skip the
+            # chunks whose OR changes nothing, so a call on an already closed
+            # matrix does less work: every timed call starts from the raw
+            # graph, restored from a pristine device copy outside the timing.
             self.A = inputs.make_tc_input(self.spec)
             self.dA = self.A.cuda()
+            self.raw = self.dA.clone()
             return
         if self.spec["kind"] == "poly":
             self.A, self.B = inputs.make_poly_inputs(self.spec)     # coefficients, points
@@ -179,6 +190,13 @@ class Workload:
             self.C = torch.empty(c_shape, dtype=inputs.TORCH_DTYPE[self.spec["out"]],
                                  device="cuda")
         self.s = self.spec["s"]
+
+    def restore(self):
+        """Put the raw input back (the in-place closure only; else None)."""
+        self.dA.copy_(self.raw)
+
+    def needs_restore(self) -> bool:
+        return self.spec["kind"] == "tc"
 
     def call(self):
         sp = self.spec
@@ -201,7 +219,7 @@ class Workload:
 SETTLE_S = 0.3
 
 
-def settle(fn, seconds: float = SETTLE_S) -> None:
+def settle(fn, seconds: float = SETTLE_S, restore=None) -> None:
     """Run the call back to back for `seconds` (untimed) so the GPU leaves
     its idle clock state: after the host-side input generation the device has
     been idle, and the first milliseconds of work run measurably slower."""
@@ -209,36 +227,58 @@ def settle(fn, seconds: float = SETTLE_S) -> None:
     t0 = time.perf_counter()
     while time.perf_counter() - t0 < seconds:
         for _ in range(8):
+            if restore is not None:
+                restore()
             fn()
         torch.cuda.synchronize()
 
 
-def time_steps(fn, steps: int, warmup: int) -> float:
-    """Average ms per call over `steps` back-to-back calls, timed with HIP
-    events on the current stream (the stream the library launches on),
-    after a clock-settling period and `warmup` untimed calls."""
+def time_steps(fn, steps: int, warmup: int, restore=None) -> float:
+    """Average ms per call over `steps` calls, timed with HIP events on the
+    current stream (the stream the library launches on), after a
+    clock-settling period and `warmup` untimed calls.  Without `restore` the
+    calls run back to back between one pair of events; with it, every call
+    is preceded by restore() (putting an in-place call's input back) outside
+    its own pair of events, and the per-call times are summed."""
     import torch
-    settle(fn)
+    settle(fn, restore=restore)
     for _ in range(warmup):
+        if restore is not None:
+            restore()
         fn()
     torch.cuda.synchronize()
     st = torch.cuda.current_stream()
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
-    e0.record(st)
+    if restore is None:
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(st)
+        for _ in range(steps):
+            fn()
+        e1.record(st)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps
+    pairs = []
     for _ in range(steps):
+        restore()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(st)
         fn()
-    e1.record(st)
+        e1.record(st)
+        pairs.append((e0, e1))
     torch.cuda.synchronize()
-    return e0.elapsed_time(e1) / steps
+    return sum(a.elapsed_time(b) for a, b in pairs) / steps
 
 
 def measure(name: str, steps: int, warmup: int) -> dict:
     w = Workload(name)
     tcu = w.tcu
     tcu.tcu_set_unit(w.s)
-    ms = time_steps(w.call, steps, warmup)
+    restore = w.restore if w.needs_restore() else None
+    ms = time_steps(w.call, steps, warmup, restore=restore)
     tcu.tcu_reset_calls()
+    if restore is not None:
+        restore()
     w.call()
     import torch
     torch.cuda.synchronize()
@@ -294,65 +334,186 @@ def measure(name: str, steps: int, warmup: int) -> dict:
     return out
 
 
-def ell_fit(steps: int = 200) -> dict:
-    """Per-call latency l: least-squares intercept of t(n) = a*n + l over
-    native bf16 -> bf16 calls with s = 32 (the model's O(n sqrt(m) + l))."""
+# (dtype code, unit size) of the native calls whose cost is fitted, keyed by
+# the (input, output) types of the configured workloads.
+ELL_CASES = {("f16", "f32"): 16, ("bf16", "f32"): 32, ("bf16", "bf16"): 32, ("i8", "i32"): 32}
+ELL_ROWS = [16, 32, 256, 1024, 4096, 16384, 65536, 262144, 1048576, 4194304, 16777216]
+
+
+def _timing_lib():
+    import ctypes
+    from paper_1908_06649_amd import build as hip_build
+    if not os.path.exists(hip_build.TIMING_LIB):
+        raise RuntimeError(f"{hip_build.TIMING_LIB} is missing: build the library first")
+    lib = ctypes.CDLL(hip_build.TIMING_LIB)
+    fn = lib.tcu_timing_tall_loop
+    fn.restype = ctypes.c_int
+    fn.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_void_p,
+                   ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int,
+                   ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]
+    return fn
+
+
+def ell_fit() -> dict:
+    """The model's cost of one native call, O(n sqrt(m) + l) (Section 3),
+    fitted per (input, output) type and unit size as t(n) = a*(n*s) + l: a
+    in seconds per unit of model work, l the per-call latency.  Times come
+    from a loop in C (libtcu_timing.so) issuing tcu_mm_tall_ex back to back
+    on torch's current stream, so no Python marshalling is in them; the fit
+    weights each point by 1/t (relative residuals), so the small-n points fix
+    l and the large-n points fix a.  Also reported: the round trip of one
+    synchronised call, and the Python binding's per-call time at the
+    smallest n for comparison."""
+    import ctypes
     import numpy as np
     import torch
-    from paper_1908_06649_amd import tcu
-    s = 32
-    ns = [32, 1024, 4096, 16384, 65536, 262144, 1048576]
-    A = torch.randn(ns[-1], s, device="cuda").to(torch.bfloat16)
-    B = torch.randn(s, s, device="cuda").to(torch.bfloat16)
-    C = torch.empty(ns[-1], s, device="cuda", dtype=torch.bfloat16)
-    tcu.tcu_set_unit(s)
-    ts = []
-    for n in ns:
-        a, c = A[:n], C[:n]
-        ts.append(time_steps(lambda: tcu.tcu_mm_tall(a, n, s, B, c), steps, 10) * 1e3)
-    slope, icpt = np.polyfit(np.array(ns, dtype=float), np.array(ts), 1)
-    return {"n": ns, "us_per_call": [round(t, 3) for t in ts],
-            "fit_us_per_row": float(slope), "ell_us": float(icpt)}
+    from paper_1908_06649_amd import inputs, tcu
+    loop = _timing_lib()
+    st = torch.cuda.current_stream().cuda_stream
+    codes = {("f16", "f32"): tcu.TCU_F16_F32, ("bf16", "f32"): tcu.TCU_BF16_F32,
+             ("bf16", "bf16"): tcu.TCU_BF16_BF16, ("i8", "i32"): tcu.TCU_I8_I32}
+    out = {}
+    for (din, dout), s in ELL_CASES.items():
+        ns = [n for n in ELL_ROWS if n >= s]
+        nmax = ns[-1]
+        g = torch.Generator().manual_seed(99)
+        A = inputs.draw((nmax, s), din, "int8" if din == "i8" else "normal", g).cuda()
+        B = inputs.draw((s, s), din, "int8" if din == "i8" else "normal", g).cuda()
+        C = torch.empty(nmax, s, dtype=inputs.TORCH_DTYPE[dout], device="cuda")
+        ts, tsync = [], []
+        settle(lambda: tcu.tcu_mm_tall_ex(A, nmax, s, B, C), 0.2)
+        for n in ns:
+            reps = max(20, min(2000, int(2e7 // (n * s))))
+            a_t, s_t = ctypes.c_double(), ctypes.c_double()
+            rc = loop(A.data_ptr(), n, s, B.data_ptr(), C.data_ptr(), codes[(din, dout)], st,
+                      reps, ctypes.byref(a_t), ctypes.byref(s_t))
+            if rc != 0:
+                raise RuntimeError(f"timing loop failed: {tcu.tcu_strerror(rc)}")
+            ts.append(a_t.value)
+            tsync.append(s_t.value)
+        x = np.array(ns, dtype=float) * s
+        y = np.array(ts)
+        w = 1.0 / y
+        slope, icpt = np.polyfit(x, y, 1, w=w)
+        n0 = ns[0]
+        a0, c0 = A[:n0], C[:n0]
+        py_ms = time_steps(lambda: tcu.tcu_mm_tall_ex(a0, n0, s, B, c0), 500, 20)
+        out[f"{din}_{dout}_s{s}"] = {
+            "s": s, "n": ns, "us_per_call_async": [round(t * 1e6, 3) for t in ts],
+            "us_per_call_sync": [round(t * 1e6, 3) for t in tsync],
+            "a_s_per_work": float(slope), "ell_us": float(icpt) * 1e6,
+            "python_binding_us_per_call_at_min_n": py_ms * 1e3}
+        del A, B, C
+        torch.cuda.empty_cache()
+    return out
 
 
-def cpu_baseline(w: "Workload", target_s: float = 15.0) -> dict:
-    """Time the CPU oracle on a bounded sample of the headline product:
-    R of the N output rows (2*R*N^2 flops), R sized for ~target_s seconds.
-    The sampled rows are also compared with the GPU result."""
+def model_time(spec: dict, calls: int, work: int, ms: float, fits: dict) -> dict | None:
+    """Theorem 2's (and the native call's) model time for one call of the
+    workload -- T = a * (model work) + (calls) * l, with a and l fitted for
+    its types and unit size (ell_fit) -- against the measured time."""
+    key = f"{spec.get('dtype')}_{spec.get('out')}_s{spec.get('s')}"
+    f = fits.get(key)
+    if f is None:
+        return None
+    t_model = f["a_s_per_work"] * work + calls * f["ell_us"] * 1e-6
+    form = ("N^3/s + (N/s)^2 l" if spec["kind"] == "gemm" else
+            "n s + l" if spec["kind"] == "tall" else "work + calls l")
+    return {"form": form, "fit": key, "model_work": work, "calls": calls,
+            "a_s_per_work": f["a_s_per_work"], "ell_us": f["ell_us"],
+            "T_model_ms": t_model * 1e3, "measured_ms": ms,
+            "measured_over_model": (ms * 1e-3) / t_model if t_model > 0 else None}
+
+
+def host_info() -> dict:
+    """The machine the CPU oracle runs on."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        affinity = len(os.sched_getaffinity(0))
+    except AttributeError:
+        affinity = None
+    import oracle
+    return {"cpu_model": model, "nproc": os.cpu_count(), "affinity_cpus": affinity,
+            "OMP_NUM_THREADS": os.environ.get("OMP_NUM_THREADS"),
+            "oracle_threads": oracle.threads()}
+
+
+def cpu_baseline(w: "Workload", target_s: float = 15.0) -> dict | None:
+    """Time the CPU oracle on a bounded sample of the workload just measured
+    and compare the GPU result with it on that sample.
+      product / native call: R of the output rows (R rows of A times B), R
+        sized from two probes for ~target_s seconds (all rows when they fit);
+      closure: the whole closure (bit sets, the section's iterative
+        algorithm), compared exactly.
+    Parity on the sample: bit-exact for int8, else the relative Frobenius,
+    elementwise and (bfloat16 output) rounding bounds of oracle/compare."""
     import numpy as np
     import oracle
     from oracle import compare
     from paper_1908_06649_amd import inputs
     sp = w.spec
-    N, dt = sp["N"], sp["dtype"]
+    if sp["kind"] == "tc":
+        d = w.A.numpy()
+        t0 = time.perf_counter()
+        ref = oracle.transitive_closure(d)
+        secs = time.perf_counter() - t0
+        got = w.dA.cpu().numpy().view(np.uint8)
+        mism = int((got != ref).sum())
+        assert mism == 0, f"closure differs from the oracle in {mism} entries"
+        n = sp["n"]
+        return {"value": 2.0 * n ** 3 / secs / 1e12, "unit": "boolean TOP/s",
+                "cores": oracle.threads(), "kind": "oracle",
+                "sample": f"the whole closure of the {n}-vertex graph, bit-set rows",
+                "seconds": secs, "parity": {"mismatches": 0}}
+    if sp["kind"] not in ("gemm", "tall"):
+        return None
+    dt, out = sp["dtype"], sp["out"]
     Ab, Bb = inputs.bits(w.A), inputs.bits(w.B)
+    rows_total, K = Ab.shape
+    J = Bb.shape[1]
     rng = np.random.default_rng(123)
     # two probes separate the per-call setup (decoding B) from the per-row cost
     t_probe = []
     for k in (8, 40):
-        rows_p = np.sort(rng.choice(N, k, replace=False))
+        k = min(k, rows_total)
+        rows_p = np.sort(rng.choice(rows_total, k, replace=False))
         t0 = time.perf_counter()
         oracle.mm(Ab, Bb, dt, rows=rows_p)
         t_probe.append(time.perf_counter() - t0)
     per_row = max((t_probe[1] - t_probe[0]) / 32, 1e-9)
     fixed = max(t_probe[0] - 8 * per_row, 0.0)
-    R = int(max(8, min(N, (target_s - fixed) / per_row)))
-    rows = np.sort(rng.choice(N, R, replace=False))
+    R = int(max(8, min(rows_total, (target_s - fixed) / per_row)))
+    rows = None if R >= rows_total else np.sort(rng.choice(rows_total, R, replace=False))
+    R = rows_total if rows is None else R
     t0 = time.perf_counter()
     ref = oracle.mm(Ab, Bb, dt, rows=rows)
     secs = time.perf_counter() - t0
-    got = w.C[rows].cpu()
-    got = got.numpy()
+    Cg = w.C.view(rows_total, J)
+    got = Cg if rows is None else Cg[rows]
+    got = got.cpu()
+    got = got.view(__import__("torch").int16).numpy().view(np.uint16) if out == "bf16" \
+        else got.numpy()
     if dt == "i8":
         parity = compare.check_exact(got, ref)
     else:
         absab = oracle.mm(compare.abs_bits(Ab), compare.abs_bits(Bb), dt, rows=rows)
-        parity = compare.check_float(got, ref, absab)
-    flops = 2.0 * R * N * N
+        parity = (compare.check_bf16(got, ref, absab, K=K) if out == "bf16"
+                  else compare.check_float(got, ref, absab))
+    flops = 2.0 * R * K * J
+    what = (f"{sp['N']}x{sp['N']} {dt} product" if sp["kind"] == "gemm"
+            else f"{rows_total}x{K} by {K}x{J} {dt} native call")
     return {"value": flops / secs / 1e12, "unit": "TOP/s" if dt == "i8" else "TFLOP/s",
             "cores": oracle.threads(), "kind": "oracle",
-            "sample": f"{R} of {N} output rows of the {N}x{N} {dt} product "
-                      f"({flops:.3e} flop), binary64/int64 triple loop",
+            "sample": f"{R} of {rows_total} output rows of the {what} ({flops:.3e} "
+                      f"{'op' if dt == 'i8' else 'flop'}), binary64/int64 triple loop",
             "seconds": secs, "parity_sampled_rows": parity}
 
 
@@ -442,13 +603,21 @@ def main() -> int:
         cost["calls_theorem2_and_lower_bound"] = main_res["calls_theorem2"]
     elif sp["kind"] == "rect":
         cost["calls_corollary1"] = main_res["calls_corollary1"]
-    if not args.no_cpu_baseline and sp["kind"] == "gemm":
+    if not args.no_cpu_baseline and sp["kind"] in ("gemm", "tall", "tc"):
         result["cpu_baseline"] = cpu_baseline(w)
+        result["host"] = host_info()
     else:
         result["cpu_baseline"] = None
     del w
     torch.cuda.empty_cache()
 
+    fits = ell_fit() if not args.no_secondary else {}
+    if fits:
+        cost["ell_fit"] = fits
+        mt = model_time(sp, main_res["calls"], main_res["model_work"], main_res["ms_per_call"],
+                        fits)
+        if mt is not None:
+            cost["model_time"] = {args.workload: mt}
     if not args.no_secondary:
         sec = {}
         for name in inputs.WORKLOADS:
@@ -457,12 +626,17 @@ def main() -> int:
             spec = inputs.WORKLOADS[name]
             steps = args.steps if spec.get("N", 0) >= 8192 or spec.get("n", 0) >= 1 << 20 else 200
             r = measure(name, steps, max(args.warmup, 5))
-            r.pop("_workload")
+            rw = r.pop("_workload")
             sec[name] = {k: r[k] for k in ("value", "unit", "ms_per_call", "roofline", "calls",
                                            "square_calls", "model_work")}
+            mt = model_time(spec, r["calls"], r["model_work"], r["ms_per_call"], fits)
+            if mt is not None:
+                cost.setdefault("model_time", {})[name] = mt
+            if not args.no_cpu_baseline:
+                sec[name]["cpu_baseline"] = cpu_baseline(rw)
+            del rw
             torch.cuda.empty_cache()
         result["secondary"] = sec
-        cost["ell_fit"] = ell_fit()
     if not args.no_rect:
         rect = {}
         for name in inputs.RECT_WORKLOADS:
@@ -492,10 +666,15 @@ def main() -> int:
             if name == args.workload:
                 continue
             r = measure(name, args.steps, max(args.warmup, 5))
-            r.pop("_workload")
+            rw = r.pop("_workload")
             tc[name] = {k: r[k] for k in ("value", "unit", "ms_per_call", "roofline", "bool_tops",
                                           "calls", "calls_section43", "square_calls",
                                           "model_work")}
+            tc[name]["timing"] = "each timed call starts from the raw graph (restored outside " \
+                                 "the timed region)"
+            if not args.no_cpu_baseline:
+                tc[name]["cpu_baseline"] = cpu_baseline(rw)
+            del rw
             torch.cuda.empty_cache()
         result["tc"] = tc
     if not args.no_dft:

@@ -38,6 +38,14 @@
  *     overlap) all run before any HIP call, so a rejected call touches no
  *     device state.  A rejected call leaves C unmodified and does not count
  *     as a tensor-unit call.
+ *   - The library cannot tell a device pointer from a host or stale one by
+ *     its value: a kernel given such a pointer faults the GPU.  With pointer
+ *     checks on (TCU_KNOB_CHECK_POINTERS, or the environment variable
+ *     TCU_DEBUG set to a nonzero integer when the library is loaded), every
+ *     entry point first asks the HIP runtime whether each operand's whole
+ *     extent lies inside one device allocation of the current device, and
+ *     returns TCU_ERR_POINTER, before any launch, if not.  The check costs a
+ *     few runtime queries per call and is off by default.
  *   - Base pointers must be 16-byte aligned.  C must not overlap A or B
  *     (A and B may overlap each other; both are only read).
  *   - Unit configuration (tcu_set_unit, tcu_set_dtype, tcu_set_stream) is
@@ -60,7 +68,9 @@ typedef enum tcu_status {
     TCU_ERR_ALIGN = -4,       /* a base pointer is not 16-byte aligned */
     TCU_ERR_OVERLAP = -5,     /* C overlaps A or B */
     TCU_ERR_HIP = -6,         /* the HIP runtime reported an error (launch, device query) */
-    TCU_ERR_NO_DEVICE = -7    /* no HIP device is visible */
+    TCU_ERR_NO_DEVICE = -7,   /* no HIP device is visible */
+    TCU_ERR_POINTER = -8      /* pointer checks on: an operand is not inside one device
+                                 allocation of the current device (tcu_check_device_range) */
 } tcu_status;
 
 /* Element types (input, output) of the unit.  Floating-point inputs are
@@ -125,7 +135,16 @@ int tcu_mm_tall(const void *A, int64_t n, int s, const void *B, void *C);
  *   N: order; s <= N <= TCU_MAX_ORDER and N % s == 0, s = tcu_get_unit().
  * Errors: as tcu_mm_tall, with TCU_ERR_SHAPE for N < s or N % s != 0.
  * On success the logical call counter advances by (N/s)^2 = n/m, the number
- * of calls of Theorem 2 (and its lower bound on right-matrix loads). */
+ * of calls of Theorem 2 (and its lower bound on right-matrix loads).
+ * Reproducibility: int32 and bfloat16 results are the same on every call.
+ * A binary32 result is too, unless the product splits the contracted index
+ * across workgroups -- which it does when the 256 x 256 output tiles are
+ * fewer than the device's compute units, or when they do not fill a whole
+ * number of rounds of the persistent grid (the tiles of the last round are
+ * then split) -- because the partial sums are then added into C with atomic
+ * additions in no fixed order: the low bits of such a binary32 result may
+ * differ from call to call (each result is within the stated summation
+ * bound; the order-8192 products are not split). */
 int tcu_gemm(const void *A, const void *B, void *C, int64_t N);
 
 /* Stateless forms of the two calls: unit size, dtype and stream are
@@ -170,7 +189,10 @@ int tcu_gemm_ex(const void *A, const void *B, void *C, int64_t N, int s,
  * same type and the result is stored once (rounded to nearest even for a
  * bfloat16 output).  For int8 inputs K < 2^17 is required, so A*B is exact
  * in int32; the accumulated C + A*B wraps modulo 2^32 if it leaves the
- * int32 range.
+ * int32 range.  As for tcu_gemm, a binary32 result whose contracted index
+ * is split across workgroups (few output tiles with a long K, or the tiles
+ * of a partial last round) is summed in no fixed order, so its low bits may
+ * differ from call to call; int32 and bfloat16 results are reproducible.
  * Layout rules: base pointers 16-byte aligned; every element each operand
  * addresses must lie below 2^40 bytes from its base.  Row pitches need no
  * alignment, but pitches whose byte size is a multiple of 16 (lda, ldb, ldc
@@ -201,9 +223,13 @@ int tcu_gemm_rect_ex(const void *A, int64_t lda, const void *B, int64_t ldb, voi
  * (the coefficients read column-major), cut into s x s blocks -- ceil(n/m)
  * tall calls of p rows -- followed by A(x_i) = sum_j C[i][j] x_i^(js).
  * The powers are formed in binary32 and handed to the unit as the sum of
- * two words of the input type (X = X_hi + X_lo), so every call is issued
- * twice; the combine runs in binary32 and C is never stored.  n and p need
- * not be multiples of s (zero padding; the theorem assumes them).
+ * two bfloat16 words (X = X_hi + X_lo, about 2^-17 relative accuracy), so
+ * every call is issued twice; binary16 coefficients are split exactly into
+ * two bfloat16 words each (c = c_hi + c_lo), so with binary16 inputs every
+ * call is issued four times -- bfloat16 has binary32's exponent range, so
+ * small powers x^k do not underflow as binary16 words would.  The combine
+ * runs in binary32 and C is never stored.  n and p need not be multiples of
+ * s (zero padding; the theorem assumes them).
  *   coef: n input elements (binary16 or bfloat16, the unit's input type).
  *   n: number of coefficients (degree n-1); 0 <= n <= TCU_MAX_ROWS; n = 0
  *      gives zeros.
@@ -213,14 +239,16 @@ int tcu_gemm_rect_ex(const void *A, int64_t lda, const void *B, int64_t ldb, voi
  *      bfloat16 rounded once to nearest even (TCU_BF16_BF16).
  * The unit size and dtype come from tcu_get_unit() / tcu_get_dtype()
  * (TCU_I8_I32 is TCU_ERR_UNSUPPORTED).  Results are meaningful while
- * |x|^(n-1) and the partial sums stay in binary32 range (the theorem
- * assumes no overflow) and, for binary16 inputs, |x|^k < 65504 for
- * k < min(n, s).
+ * |x|^(n-1) and the partial sums stay in binary32's normal range (the
+ * theorem assumes evaluation without overflow; a term a_h x^h whose powers
+ * fall below about 2^-118 loses relative accuracy to binary32 and bfloat16
+ * underflow).
  * A pointer may be NULL only if its array is empty.  Errors: TCU_ERR_NULL,
  * TCU_ERR_SHAPE, TCU_ERR_UNSUPPORTED, TCU_ERR_ALIGN (16-byte base
  * alignment), TCU_ERR_OVERLAP (out overlapping coef or points),
  * TCU_ERR_NO_DEVICE, TCU_ERR_HIP.
- * Cost accounting: 2*ceil(n/m) calls of ceil(p/s) square calls each. */
+ * Cost accounting: 2*ceil(n/m) calls (4*ceil(n/m) for binary16 inputs)
+ * of ceil(p/s) square calls each. */
 int tcu_poly_eval(const void *coef, int64_t n, const void *points, int64_t p, void *out);
 int tcu_poly_eval_ex(const void *coef, int64_t n, const void *points, int64_t p, void *out, int s,
                      int dtype, void *hip_stream);
@@ -276,7 +304,6 @@ int tcu_transitive_closure_ex(void *X, int64_t n, int64_t ld, int s, void *hip_s
 int tcu_dft(const void *x, void *y, void *work, int64_t n, int64_t batch);
 int tcu_dft_ex(const void *x, void *y, void *work, int64_t n, int64_t batch, int s,
                void *hip_stream);
-
 /* ---- cost accounting (Theorem 2 proof; Section 5 weak model) ----
  * tcu_calls:        logical tensor-unit calls issued (1 per tall call,
  *                   (N/s)^2 per tcu_gemm).
@@ -292,6 +319,51 @@ void tcu_reset_calls(void);
 
 /* Static, human-readable text for a status code. */
 const char *tcu_strerror(int status);
+
+/* ---- pointer checks and test overrides ----
+ *
+ * tcu_check_device_range: TCU_OK if bytes == 0, or if [p, p + bytes) lies
+ * inside one device (or managed) allocation of the current HIP device;
+ * TCU_ERR_POINTER if p is a host pointer, unknown to the runtime, on
+ * another device, or the range runs past its allocation (with torch's
+ * caching allocator: past the cached block holding it); TCU_ERR_SHAPE for
+ * bytes < 0; TCU_ERR_NO_DEVICE / TCU_ERR_HIP if the runtime cannot answer.
+ * A failed query leaves HIP's last-error state as it was before the call.
+ * This is the check every entry point applies to each operand while
+ * TCU_KNOB_CHECK_POINTERS is 1.
+ *
+ * tcu_set_knob / tcu_get_knob: process-wide overrides of the library's
+ * automatic choices, for tests that must reach every kernel path on small
+ * shapes, and the pointer-check switch.  Value 0 restores the automatic
+ * choice.  Products never read the environment; only the initial value of
+ * TCU_KNOB_CHECK_POINTERS comes from TCU_DEBUG at load time.
+ *   TCU_KNOB_GEMM_KERNEL: TCU_PATH_AUTO, TCU_PATH_FULL_TILE (the 256 x 256
+ *     persistent kernel wherever its shape conditions hold),
+ *     TCU_PATH_GENERAL (the general kernel), TCU_PATH_RING (the small-tile
+ *     ring kernel where its shape conditions hold).
+ *   TCU_KNOB_PP_GRID: workgroups of the persistent full-tile kernel (0: one
+ *     per compute unit).
+ *   TCU_KNOB_SPLIT_K: forced number of contracted-index ranges of a
+ *     full-tile product with binary32/int32 output (0: by size).
+ *   TCU_KNOB_TAIL_SPLIT: forced number of ranges of the last round's tiles
+ *     (0: by size; 1: none).
+ *   TCU_KNOB_CHECK_POINTERS: 1 = check every operand with
+ *     tcu_check_device_range before launching, 0 = no checks.
+ * Returns TCU_OK, or TCU_ERR_UNSUPPORTED for an unknown knob or a value
+ * out of range (the knob is then unchanged); tcu_get_knob returns -1 for an
+ * unknown knob.  Changing a knob while another thread issues calls is safe
+ * but gives that thread either value. */
+enum {
+    TCU_KNOB_GEMM_KERNEL = 0,
+    TCU_KNOB_PP_GRID = 1,
+    TCU_KNOB_SPLIT_K = 2,
+    TCU_KNOB_TAIL_SPLIT = 3,
+    TCU_KNOB_CHECK_POINTERS = 4
+};
+enum { TCU_PATH_AUTO = 0, TCU_PATH_FULL_TILE = 1, TCU_PATH_GENERAL = 2, TCU_PATH_RING = 3 };
+int tcu_check_device_range(const void *p, int64_t bytes);
+int tcu_set_knob(int knob, int value);
+int tcu_get_knob(int knob);
 
 #ifdef __cplusplus
 }

@@ -132,15 +132,19 @@ def check(dtype_in: str, dtype_out: str, A_bits, B_bits, got, rows=None, C0=None
 def poly_bound(dtype_in: str, n: int, s: int) -> float:
     """Relative-to-magnitude error bound of the batch polynomial evaluation
     (Theorem 11) as the unit computes it, times a safety factor of 4:
-      * X = X_hi + X_lo leaves a residual of at most 2^-18 |x^k| (bfloat16:
-        two nearest roundings of 9 significant bits) or 2^-22 (binary16);
+      * X = X_hi + X_lo as two bfloat16 words (for both input types; the
+        binary16 coefficients are split exactly into two bfloat16 words)
+        leaves a residual of at most 2^-18 |x^k| (two nearest roundings of
+        9 significant bits);
       * every power is a chain of at most 2 log2(s) + s binary32 products,
         the block weights y^(s J) a chain of n/s^2 more;
       * the unit's sums run over s products, the combine over s + n/s^2
         terms plus two cross-lane additions;
     each binary32 operation adding at most 2^-24 of the magnitude sum
     sum_h |a_h| |x|^h."""
-    split = 2.0 ** -18 if dtype_in == "bf16" else 2.0 ** -22
+    if dtype_in not in ("f16", "bf16"):
+        raise ValueError("polynomial evaluation takes f16 or bf16 inputs")
+    split = 2.0 ** -18
     ops = 2 * 6 + s + s + 2 * (n // (s * s) + 1) + 8
     return 4.0 * (split + ops * 2.0 ** -24)
 

@@ -13,6 +13,9 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libtcu.so")
+# The benchmark's host-side timing loop (calls libtcu.so through the C ABI).
+TIMING_SRC = "tcu_timing.cpp"
+TIMING_LIB = os.path.join(HERE, "libtcu_timing.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
 SOURCES = ["tcu_abi.cpp", "tcu_tall.hip", "tcu_gemm.hip", "tcu_poly.hip", "tcu_tc.hip",
            "tcu_dft.hip"]
@@ -57,6 +60,16 @@ def build(verbose: bool = False) -> str:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
     os.replace(tmp, LIB)
+    tmp = TIMING_LIB + ".tmp"
+    cmd = [hipcc(), "-O2", "-std=c++17", "-fPIC", "-shared", f"-I{INCLUDE}",
+           os.path.join(CSRC, TIMING_SRC), f"-L{HERE}", "-ltcu", "-Wl,-rpath,$ORIGIN",
+           "-o", tmp]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        raise RuntimeError(f"hipcc failed for {TIMING_SRC}:\n{res.stdout}\n{res.stderr}")
+    os.replace(tmp, TIMING_LIB)
     return LIB
 
 

@@ -5,8 +5,12 @@
 
 #include <atomic>
 #include <cstdint>
+#include <cstdlib>
 #include <cstring>
 #include <mutex>
+
+#include <initializer_list>
+#include <utility>
 
 #include "tcu.h"
 #include "tcu_launch.h"
@@ -23,6 +27,17 @@ struct UnitConfig {
   void *stream = nullptr;
 };
 thread_local UnitConfig g_cfg;
+
+// Test overrides and the pointer-check switch (tcu_set_knob).  Pointer
+// checks start on when TCU_DEBUG holds a nonzero integer at load time; the
+// environment is read only here, once.
+constexpr int kKnobs = 5;
+int initial_knob(int k) {
+  if (k != TCU_KNOB_CHECK_POINTERS) return 0;
+  const char *v = std::getenv("TCU_DEBUG");
+  return v && std::atoi(v) != 0 ? 1 : 0;
+}
+std::atomic<int> g_knob[kKnobs] = {{0}, {0}, {0}, {0}, {initial_knob(TCU_KNOB_CHECK_POINTERS)}};
 
 std::atomic<int64_t> g_calls{0};
 std::atomic<int64_t> g_square_calls{0};
@@ -73,6 +88,45 @@ int device_ready(int *num_cus) {
   }
   if (d.state < 0) return d.state;
   *num_cus = d.num_cus;
+  return TCU_OK;
+}
+
+// Whether [p, p + bytes) lies inside one device allocation of the current
+// device (tcu_check_device_range).  A failed query's error is cleared from
+// HIP's last-error state unless that state already held an error.
+int device_range(const void *p, int64_t bytes) {
+  if (bytes < 0) return TCU_ERR_SHAPE;
+  if (bytes == 0) return TCU_OK;
+  if (!p) return TCU_ERR_POINTER;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return TCU_ERR_HIP;
+  const hipError_t before = hipPeekAtLastError();
+  auto fail = [&](int status) {
+    if (before == hipSuccess) (void)hipGetLastError();
+    return status;
+  };
+  hipPointerAttribute_t attr;
+  std::memset(&attr, 0, sizeof(attr));
+  if (hipPointerGetAttributes(&attr, p) != hipSuccess) return fail(TCU_ERR_POINTER);
+  if ((attr.type != hipMemoryTypeDevice && attr.type != hipMemoryTypeManaged) ||
+      attr.device != dev)
+    return TCU_ERR_POINTER;
+  hipDeviceptr_t base = nullptr;
+  size_t size = 0;
+  if (hipMemGetAddressRange(&base, &size, const_cast<void *>(p)) != hipSuccess)
+    return fail(TCU_ERR_POINTER);
+  const uintptr_t b = reinterpret_cast<uintptr_t>(base), q = reinterpret_cast<uintptr_t>(p);
+  if (q < b || q - b > size || (uint64_t)bytes > size - (q - b)) return TCU_ERR_POINTER;
+  return TCU_OK;
+}
+
+// With pointer checks on, every operand extent (pointer, bytes) in turn.
+int check_ranges(std::initializer_list<std::pair<const void *, int64_t>> ranges) {
+  if (g_knob[TCU_KNOB_CHECK_POINTERS].load(std::memory_order_relaxed) == 0) return TCU_OK;
+  for (const auto &r : ranges) {
+    const int rc = device_range(r.first, r.second);
+    if (rc != TCU_OK) return rc;
+  }
   return TCU_OK;
 }
 
@@ -192,19 +246,49 @@ int validate_tc(const void *X, int64_t n, int64_t ld, int s) {
   return TCU_OK;
 }
 
-int validate_dft(const void *x, const void *y, const void *work, int64_t n, int64_t batch, int s) {
+// The DFT's checks other than its work buffer: unit size, n, batch,
+// extent, x and y (null, alignment, overlap).  *need_work: whether the
+// transform has more than one level (its levels then need a second buffer).
+int validate_dft_xy(const void *x, const void *y, int64_t n, int64_t batch, int s,
+                    bool *need_work) {
   if (!unit_ok(s)) return TCU_ERR_UNSUPPORTED;
   if (n < 1 || n > TCU_MAX_DFT_N || (n & (n - 1)) != 0 || batch < 0) return TCU_ERR_SHAPE;
   // batch * n * 8 bytes must stay below 2^40
   if (batch > 0 && n > (((int64_t)1 << 40) - 1) / 8 / batch) return TCU_ERR_SHAPE;
   const int64_t bytes = batch * n * 8;
-  const bool need_work = tcu::dft_levels(n, s) > 1;
-  if (bytes > 0 && (!x || !y || (need_work && !work))) return TCU_ERR_NULL;
-  if (misaligned(x) || misaligned(y) || misaligned(work)) return TCU_ERR_ALIGN;
+  *need_work = tcu::dft_levels(n, s) > 1;
+  if (bytes > 0 && (!x || !y)) return TCU_ERR_NULL;
+  if (misaligned(x) || misaligned(y)) return TCU_ERR_ALIGN;
   if (overlap(y, bytes, x, bytes)) return TCU_ERR_OVERLAP;
+  return TCU_OK;
+}
+
+int validate_dft(const void *x, const void *y, const void *work, int64_t n, int64_t batch, int s) {
+  bool need_work = false;
+  const int rc = validate_dft_xy(x, y, n, batch, s, &need_work);
+  if (rc != TCU_OK) return rc;
+  const int64_t bytes = batch * n * 8;
+  if (bytes > 0 && need_work && !work) return TCU_ERR_NULL;
+  if (misaligned(work)) return TCU_ERR_ALIGN;
   if (need_work && (overlap(work, bytes, x, bytes) || overlap(work, bytes, y, bytes)))
     return TCU_ERR_OVERLAP;
   return TCU_OK;
+}
+
+// Theorem 7's cost accounting of one transform of `batch` vectors.
+void count_dft(int64_t n, int64_t batch, int s) {
+  const int L = tcu::dft_levels(n, s);
+  int64_t P = 1, calls = 0, squares = 0;
+  for (int t = 1; t <= L; ++t) {
+    const int64_t R = t < L ? s : n / P;
+    const int64_t rows = n / R;
+    calls += 4 * batch;
+    squares += 4 * batch * ((rows + s - 1) / s);
+    P *= R;
+  }
+  g_calls.fetch_add(calls, std::memory_order_relaxed);
+  g_square_calls.fetch_add(squares, std::memory_order_relaxed);
+  g_work.fetch_add(squares * s * s, std::memory_order_relaxed);
 }
 
 }  // namespace
@@ -236,6 +320,9 @@ TCU_EXPORT int tcu_mm_tall_ex(const void *A, int64_t n, int s, const void *B, vo
   int num_cus = 0;
   rc = device_ready(&num_cus);
   if (rc != TCU_OK) return rc;
+  rc = check_ranges({{A, n * s * in_size(dtype)}, {B, (int64_t)s * s * in_size(dtype)},
+                     {C, n * s * out_size(dtype)}});
+  if (rc != TCU_OK) return rc;
   if (tcu::launch_tall(dtype, s, A, n, B, C, false, (hipStream_t)hip_stream, num_cus) !=
       hipSuccess)
     return TCU_ERR_HIP;
@@ -257,6 +344,9 @@ TCU_EXPORT int tcu_gemm_ex(const void *A, const void *B, void *C, int64_t N, int
   if (rc != TCU_OK) return rc;
   int num_cus = 0;
   rc = device_ready(&num_cus);
+  if (rc != TCU_OK) return rc;
+  rc = check_ranges({{A, N * N * in_size(dtype)}, {B, N * N * in_size(dtype)},
+                     {C, N * N * out_size(dtype)}});
   if (rc != TCU_OK) return rc;
   const tcu::RectArgs args{A, N, B, N, C, N, N, N, N, false};
   if (tcu::launch_rect(dtype, s, args, (hipStream_t)hip_stream, num_cus) != hipSuccess)
@@ -284,6 +374,10 @@ TCU_EXPORT int tcu_gemm_rect_ex(const void *A, int64_t lda, const void *B, int64
   if (M == 0 || N == 0 || (K == 0 && accum)) return TCU_OK;
   int num_cus = 0;
   rc = device_ready(&num_cus);
+  if (rc != TCU_OK) return rc;
+  rc = check_ranges({{A, view_extent(M, K, lda, in_size(dtype))},
+                     {B, view_extent(K, N, ldb, in_size(dtype))},
+                     {C, view_extent(M, N, ldc, out_size(dtype))}});
   if (rc != TCU_OK) return rc;
   const tcu::RectArgs args{A, lda, B, ldb, C, ldc, M, K, N, accum};
   if (tcu::launch_rect(dtype, s, args, (hipStream_t)hip_stream, num_cus) != hipSuccess)
@@ -313,12 +407,17 @@ TCU_EXPORT int tcu_poly_eval_ex(const void *coef, int64_t n, const void *points,
   int num_cus = 0;
   rc = device_ready(&num_cus);
   if (rc != TCU_OK) return rc;
+  rc = check_ranges({{coef, n * 2}, {points, p * 2}, {out, p * out_size(dtype)}});
+  if (rc != TCU_OK) return rc;
   if (tcu::launch_poly(dtype, s, coef, n, points, p, out, (hipStream_t)hip_stream, num_cus) !=
       hipSuccess)
     return TCU_ERR_HIP;
   // Theorem 11: ceil(n/m) calls of X (p x s) times an s x s coefficient
-  // block, each issued twice (X as the sum of two words of the input type).
-  const int64_t calls = 2 * ((n + (int64_t)s * s - 1) / ((int64_t)s * s));
+  // block, each issued twice (X as the sum of two bfloat16 words), and
+  // twice more for binary16 coefficients (each the sum of two bfloat16
+  // words).
+  const int64_t per_block = dtype == TCU_F16_F32 ? 4 : 2;
+  const int64_t calls = per_block * ((n + (int64_t)s * s - 1) / ((int64_t)s * s));
   const int64_t row_blocks = (p + s - 1) / s;
   g_calls.fetch_add(calls, std::memory_order_relaxed);
   g_square_calls.fetch_add(calls * row_blocks, std::memory_order_relaxed);
@@ -338,6 +437,8 @@ TCU_EXPORT int tcu_transitive_closure_ex(void *X, int64_t n, int64_t ld, int s,
   if (n == 0) return TCU_OK;
   int num_cus = 0;
   rc = device_ready(&num_cus);
+  if (rc != TCU_OK) return rc;
+  rc = check_ranges({{X, view_extent(n, n, ld, 1)}});
   if (rc != TCU_OK) return rc;
   if (tcu::launch_tc((unsigned char *)X, ld, n, (hipStream_t)hip_stream, num_cus) != hipSuccess)
     return TCU_ERR_HIP;
@@ -365,22 +466,12 @@ TCU_EXPORT int tcu_dft_ex(const void *x, void *y, void *work, int64_t n, int64_t
   int num_cus = 0;
   rc = device_ready(&num_cus);
   if (rc != TCU_OK) return rc;
+  const int64_t bytes = batch * n * 8;
+  rc = check_ranges({{x, bytes}, {y, bytes}, {work, tcu::dft_levels(n, s) > 1 ? bytes : 0}});
+  if (rc != TCU_OK) return rc;
   if (tcu::launch_dft(x, y, work, n, batch, s, (hipStream_t)hip_stream, num_cus) != hipSuccess)
     return TCU_ERR_HIP;
-  // Theorem 7: per vector and level one tall call of n/R rows times W_R, a
-  // complex product counted as the section's four real products.
-  const int L = tcu::dft_levels(n, s);
-  int64_t P = 1, calls = 0, squares = 0;
-  for (int t = 1; t <= L; ++t) {
-    const int64_t R = t < L ? s : n / P;
-    const int64_t rows = n / R;
-    calls += 4 * batch;
-    squares += 4 * batch * ((rows + s - 1) / s);
-    P *= R;
-  }
-  g_calls.fetch_add(calls, std::memory_order_relaxed);
-  g_square_calls.fetch_add(squares, std::memory_order_relaxed);
-  g_work.fetch_add(squares * s * s, std::memory_order_relaxed);
+  count_dft(n, batch, s);
   return TCU_OK;
 }
 
@@ -397,6 +488,34 @@ TCU_EXPORT void tcu_reset_calls(void) {
   g_work.store(0);
 }
 
+TCU_EXPORT int tcu_check_device_range(const void *p, int64_t bytes) {
+  if (bytes < 0) return TCU_ERR_SHAPE;
+  if (bytes == 0) return TCU_OK;
+  int num_cus = 0;
+  const int rc = device_ready(&num_cus);
+  if (rc != TCU_OK) return rc;
+  return device_range(p, bytes);
+}
+
+TCU_EXPORT int tcu_set_knob(int knob, int value) {
+  if (knob < 0 || knob >= kKnobs || value < 0) return TCU_ERR_UNSUPPORTED;
+  if (knob == TCU_KNOB_GEMM_KERNEL && value > TCU_PATH_RING) return TCU_ERR_UNSUPPORTED;
+  if (knob == TCU_KNOB_CHECK_POINTERS && value > 1) return TCU_ERR_UNSUPPORTED;
+  g_knob[knob].store(value, std::memory_order_relaxed);
+  return TCU_OK;
+}
+
+TCU_EXPORT int tcu_get_knob(int knob) {
+  if (knob < 0 || knob >= kKnobs) return -1;
+  return g_knob[knob].load(std::memory_order_relaxed);
+}
+
+namespace tcu {
+int knob(int which) {
+  return which >= 0 && which < kKnobs ? g_knob[which].load(std::memory_order_relaxed) : 0;
+}
+}  // namespace tcu
+
 TCU_EXPORT const char *tcu_strerror(int status) {
   switch (status) {
     case TCU_OK: return "success";
@@ -407,6 +526,7 @@ TCU_EXPORT const char *tcu_strerror(int status) {
     case TCU_ERR_OVERLAP: return "the output overlaps an input";
     case TCU_ERR_HIP: return "HIP runtime error";
     case TCU_ERR_NO_DEVICE: return "no HIP device visible";
+    case TCU_ERR_POINTER: return "an operand is not inside one device allocation of the current device";
   }
   return "unknown tcu status";
 }

@@ -27,42 +27,30 @@
 // C^T = B^T A^T so each lane holds 4 consecutive columns of one row of C,
 // stored as one 16-byte write.
 // Workgroup order is XCD-aware (see map_tile).
-#include <cstdlib>
-#include <cstring>
-
 #include "tcu_device.h"
 #include "tcu_launch.h"
 
 namespace tcu {
 namespace {
 
-#ifndef TCU_GROUP_M
-#define TCU_GROUP_M 2
-#endif
-#ifndef TCU_XCD_REMAP
-#define TCU_XCD_REMAP 0
-#endif
-#ifndef TCU_RING
-#define TCU_RING 5
-#endif
+// Tile rows per group of the tile order (map_tile) and LDS ring depth of
+// the full-tile kernel, both measured best on the order-8192 products.
+constexpr int kGroupM = 2;
+constexpr int kRingStages = 5;
 
 constexpr int kBKB = 128;  // bytes of the contracted index per K-step and LDS row
 
 
 __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row ^ (row >> 3)) & 7); }
 
-// Map a workgroup id to an output tile (tm, tn): groups of TCU_GROUP_M tile
+// Map a workgroup id to an output tile (tm, tn): groups of kGroupM tile
 // rows are walked column by column.  Consecutive workgroup ids are dispatched
 // round-robin over the 8 XCDs, so with groups of 2 rows each XCD's concurrent
 // workgroups cover a compact block of tiles (shared A row-panels and B
 // column-panels in its L2) while all XCDs together sweep a band of full rows
 // (B panels shared through the memory-side cache).  Measured best for N=8192
-// against larger groups and an explicit per-XCD remap (TCU_XCD_REMAP=1).
+// against larger groups and an explicit per-XCD remap of the ids.
 __device__ __forceinline__ void map_tile(int pid, int tiles_m, int tiles_n, int &tm, int &tn) {
-  const int total = tiles_m * tiles_n;
-  constexpr int kXcds = 8;
-  if (TCU_XCD_REMAP && total % kXcds == 0) pid = (pid % kXcds) * (total / kXcds) + pid / kXcds;
-  constexpr int kGroupM = TCU_GROUP_M;
   const int per_group = kGroupM * tiles_n;
   const int group = pid / per_group;
   const int first_m = group * kGroupM;
@@ -968,7 +956,8 @@ __global__ __launch_bounds__(256) void zero_tiles_kernel(unsigned char *__restri
 // instead (at least kMinStages stages each, at most grid / tail of them),
 // added into C atomically, so the last round is about 1 / nsplit as long.
 // binary32 and int32 outputs only (a bfloat16 output is rounded once from
-// the whole sum).  TCU_TAIL_SPLIT=<n> forces n ranges (tests).  Returns
+// the whole sum).  The test override TCU_KNOB_TAIL_SPLIT = n > 0 forces n
+// ranges (1: none).  Returns
 // nsplit (1: no tail split) and sets *full to the number of whole tiles.
 template <int DT>
 int tail_split(int tiles, int grid, int64_t stages, int kMinStages, int *full) {
@@ -978,8 +967,8 @@ int tail_split(int tiles, int grid, int64_t stages, int kMinStages, int *full) {
   int64_t ns = grid / tail;
   const int64_t cap = stages / kMinStages;
   if (ns > cap) ns = cap;
-  const char *tv = std::getenv("TCU_TAIL_SPLIT");
-  if (tv && std::atoi(tv) > 0) ns = std::atoi(tv) < stages ? std::atoi(tv) : stages;
+  const int forced = knob(TCU_KNOB_TAIL_SPLIT);
+  if (forced > 0) ns = forced < stages ? forced : stages;
   if (ns < 2) return 1;
   *full = tiles - tail;
   return (int)ns;
@@ -1024,16 +1013,16 @@ hipError_t launch_bool(const unsigned char *A, const unsigned char *B, unsigned 
   return hipGetLastError();
 }
 
-// Kernel selection: TCU_GEMM_KERNEL=fast forces the full-tile (ping-pong)
-// kernel wherever its shape conditions hold, =general forces the general
-// kernel; unset or =auto picks by size.
+// Kernel selection by size; the test override TCU_KNOB_GEMM_KERNEL forces
+// the full-tile (ping-pong) kernel wherever its shape conditions hold, the
+// general kernel, or the small-tile ring kernel.
 enum class GemmPath { kAuto, kFast, kGeneral, kRing };
 GemmPath gemm_path() {
-  const char *v = std::getenv("TCU_GEMM_KERNEL");
-  if (!v) return GemmPath::kAuto;
-  if (!std::strcmp(v, "fast")) return GemmPath::kFast;
-  if (!std::strcmp(v, "general")) return GemmPath::kGeneral;
-  if (!std::strcmp(v, "ring")) return GemmPath::kRing;
+  switch (knob(TCU_KNOB_GEMM_KERNEL)) {
+    case TCU_PATH_FULL_TILE: return GemmPath::kFast;
+    case TCU_PATH_GENERAL: return GemmPath::kGeneral;
+    case TCU_PATH_RING: return GemmPath::kRing;
+  }
   return GemmPath::kAuto;
 }
 
@@ -1068,7 +1057,7 @@ hipError_t launch_general(const RectArgs &a, GemmPath path, bool vec, hipStream_
   }
   // The small-tile ring kernel: 16-bit inputs, whole 64 x 64 tiles and
   // 128-byte K stages, where the general kernel would take 64 x 64 tiles
-  // (or where forced, TCU_GEMM_KERNEL=ring).
+  // (or where forced by the test override).
   if constexpr (ES == 2) {
     const bool ring_ok = path != GemmPath::kGeneral && path != GemmPath::kFast &&
                          a.M % 64 == 0 && a.N % 64 == 0 && a.K % 64 == 0 && a.K > 0 &&
@@ -1114,9 +1103,9 @@ hipError_t launch_dt(const RectArgs &a, hipStream_t stream, int num_cus) {
     nsplit = (int)(want < cap ? want : cap);
     if (nsplit < 1) nsplit = 1;
   }
-  const char *sv = std::getenv("TCU_SPLIT_K");   // tests: force a split count
-  if (sv && fast_ok && DT != TCU_BF16_BF16 && std::atoi(sv) > 0) {
-    nsplit = std::atoi(sv);
+  const int forced_split = knob(TCU_KNOB_SPLIT_K);   // test override of the count
+  if (forced_split > 0 && fast_ok && DT != TCU_BF16_BF16) {
+    nsplit = forced_split;
     if (nsplit > a.K / KE) nsplit = (int)(a.K / KE);
   }
   if (fast_ok && (path == GemmPath::kFast || nsplit > 1 ||
@@ -1129,11 +1118,10 @@ hipError_t launch_dt(const RectArgs &a, hipStream_t stream, int num_cus) {
       if (e != hipSuccess) return e;
     }
     // Persistent grid: one workgroup per CU (the LDS ring admits one), each
-    // walking tiles blockIdx, blockIdx + grid, ...  TCU_PP_GRID=<g> sets the
-    // grid size instead (tests use a tiny grid to give every workgroup many
-    // tiles).
-    const char *gv = std::getenv("TCU_PP_GRID");
-    const int want = gv && std::atoi(gv) > 0 ? std::atoi(gv) : num_cus;
+    // walking tiles blockIdx, blockIdx + grid, ...  The test override
+    // TCU_KNOB_PP_GRID sets the grid size instead (a tiny grid gives every
+    // workgroup many tiles).
+    const int want = knob(TCU_KNOB_PP_GRID) > 0 ? knob(TCU_KNOB_PP_GRID) : num_cus;
     int full = 0;
     if (nsplit == 1) {
       const int g0 = want < tm * tn ? want : tm * tn;
@@ -1146,7 +1134,7 @@ hipError_t launch_dt(const RectArgs &a, hipStream_t stream, int num_cus) {
     }
     const int items = full + (tm * tn - full) * nsplit;
     const int grid = want < items ? want : items;
-    hipLaunchKernelGGL((gemm_pp_kernel<DT, TCU_RING, false>), dim3(grid), dim3(512), 0, stream,
+    hipLaunchKernelGGL((gemm_pp_kernel<DT, kRingStages, false>), dim3(grid), dim3(512), 0, stream,
                        (const unsigned char *)a.A, (const unsigned char *)a.B,
                        (unsigned char *)a.C, (int)a.K, a.lda, a.ldb, a.ldc, a.accum ? 1 : 0,
                        tm, tn, full, nsplit, (int)a.M, (int)a.N, TileRemap{});
@@ -1184,7 +1172,7 @@ hipError_t launch_dt(const RectArgs &a, hipStream_t stream, int num_cus) {
                                (edges_in_kernel ? a.N : N0) * OB, stream, num_cus);
       if (e != hipSuccess) return e;
     }
-    hipLaunchKernelGGL((gemm_pp_kernel<DT, TCU_RING, true>), dim3(grid), dim3(512), 0, stream,
+    hipLaunchKernelGGL((gemm_pp_kernel<DT, kRingStages, true>), dim3(grid), dim3(512), 0, stream,
                        (const unsigned char *)a.A, (const unsigned char *)a.B,
                        (unsigned char *)a.C, (int)a.K, a.lda, a.ldb, a.ldc, a.accum ? 1 : 0,
                        tm, tn, full, nsplit, (int)a.M, (int)a.N, TileRemap{});

@@ -5,9 +5,15 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "tcu.h"
+
 namespace tcu {
 
 constexpr int kNoBand = 0x7fffffff;
+
+// Current value of a test override (a TCU_KNOB_* value of tcu.h), set
+// through tcu_set_knob; 0 = the automatic choice.
+int knob(int which);
 
 // Placement of a full-tile kernel's tile grid in the output: tile row tm
 // starts at m_base + 256 tm, plus skip_m once tm >= band_m (the same for

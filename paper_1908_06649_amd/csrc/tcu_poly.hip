@@ -11,15 +11,20 @@
 //   * it computes the powers of its points in binary32 (the theorem's
 //     initial exponentiation, as a ladder of squarings shared by all lanes
 //     plus a short chain per lane) and hands X to the unit as an unevaluated
-//     sum of two words of the input type, X = X_hi + X_lo, so the unit
-//     multiplies X to about 2^-16 (bfloat16) or 2^-22 (binary16) relative
-//     accuracy instead of one rounding of the input type -- the model
-//     multiplies exactly, and one 16-bit rounding of x^k would dominate
-//     the error;
+//     sum of two bfloat16 words, X = X_hi + X_lo, so the unit multiplies X
+//     to about 2^-17 relative accuracy instead of one 16-bit rounding -- the
+//     model multiplies exactly, and one rounding of x^k would dominate the
+//     error;
 //   * for every block it loads the block's weights once (16-byte contiguous
 //     runs of coefficients, shared by the wave's U chunks) and issues two
 //     matrix-core products per 16-column half (X_hi, then X_lo into the
 //     same binary32 accumulators);
+//   * binary16 inputs are driven through the unit in bfloat16 too: the
+//     5-bit exponent of a binary16 word cannot hold x^k for small |x|
+//     (x^(S-1) below 2^-14 loses bits, below 2^-25 vanishes), while bfloat16
+//     has binary32's range.  Each binary16 coefficient is split exactly into
+//     two bfloat16 words c_hi + c_lo (its 11 significant bits fit in 8 + 8),
+//     and every block takes four products, (X_hi + X_lo)(c_hi + c_lo);
 //   * lane (r, g) then holds C[point r][columns 16h + 4g + i] of the block
 //     and forms t = sum over them of C y^(16h + i), y = x^s, by Horner's
 //     rule in y; the blocks are walked last to first and combined by
@@ -29,8 +34,7 @@
 //     exchange) and one stores A(x_i).
 // Coefficients past n and points past p are zero padding.  Results are
 // meaningful while |x|^(n-1) and the partial sums stay within binary32
-// range (the theorem assumes evaluation without overflow); for binary16
-// inputs also x^k, k < min(n, s), must be representable in binary16.
+// range (the theorem assumes evaluation without overflow or underflow).
 #include "tcu_device.h"
 #include "tcu_launch.h"
 
@@ -38,9 +42,7 @@ namespace tcu {
 namespace {
 
 constexpr int kPolyThreads = 256;  // 4 waves per workgroup
-#ifndef TCU_POLY_U
-#define TCU_POLY_U 4               // 16-point chunks per wave and pass
-#endif
+constexpr int kPolyU = 4;          // 16-point chunks per wave and pass
 
 template <int DT>
 __device__ __forceinline__ float in_to_f32(unsigned bits16) {
@@ -50,24 +52,23 @@ __device__ __forceinline__ float in_to_f32(unsigned bits16) {
     return bf16_to_f32(bits16);
 }
 
-// Two binary32 values as the high ("hi") and remainder ("lo") words of the
-// input type, packed two per 32-bit word: hi = v rounded to the input type,
-// lo = (v - hi) rounded again (v - hi is exact in binary32).  bfloat16 uses
-// the round-to-nearest-even pack convert; binary16 the packed
-// round-toward-zero convert (any rounding of hi leaves an exact remainder).
-template <int DT>
-__device__ __forceinline__ void split2(float v0, float v1, unsigned &hi, unsigned &lo) {
-  if constexpr (DT == TCU_F16_F32) {
-    hi = bitcast<unsigned>(__builtin_amdgcn_cvt_pkrtz(v0, v1));
-    const float h0 = (float)bitcast<_Float16>((unsigned short)(hi & 0xffffu));
-    const float h1 = (float)bitcast<_Float16>((unsigned short)(hi >> 16));
-    lo = bitcast<unsigned>(__builtin_amdgcn_cvt_pkrtz(v0 - h0, v1 - h1));
-  } else {
-    hi = pack_bf16x2(v0, v1);
-    const float h0 = __builtin_bit_cast(float, hi << 16);
-    const float h1 = __builtin_bit_cast(float, hi & 0xffff0000u);
-    lo = pack_bf16x2(v0 - h0, v1 - h1);
-  }
+// Two binary32 values as the high ("hi") and remainder ("lo") bfloat16
+// words, packed two per 32-bit word: hi = v rounded to nearest even, lo =
+// (v - hi) rounded again (v - hi is exact in binary32), so hi + lo is v to
+// 2^-18 |v|, and exactly v when v has at most 16 significant bits.
+__device__ __forceinline__ void split_bf16(float v0, float v1, unsigned &hi, unsigned &lo) {
+  hi = pack_bf16x2(v0, v1);
+  const float h0 = __builtin_bit_cast(float, hi << 16);
+  const float h1 = __builtin_bit_cast(float, hi & 0xffff0000u);
+  lo = pack_bf16x2(v0 - h0, v1 - h1);
+}
+
+// A word of two binary16 coefficients as the exact sum of two words of
+// bfloat16 pairs (11 significant bits in 8 + 8).
+__device__ __forceinline__ void f16_pair_to_bf16(unsigned w, unsigned &hi, unsigned &lo) {
+  const float f0 = (float)bitcast<_Float16>((unsigned short)(w & 0xffffu));
+  const float f1 = (float)bitcast<_Float16>((unsigned short)(w >> 16));
+  split_bf16(f0, f1, hi, lo);
 }
 
 // b^(step * g) for lane group g = 0..3 from the ladder b^step, b^(2 step):
@@ -93,6 +94,10 @@ __global__ __launch_bounds__(kPolyThreads) void poly_kernel(const unsigned char 
   constexpr int kH = S / 16;             // 16-column halves of a block
   typedef typename std::conditional<kRun == 8, u32x4, u32x2>::type Run;
   constexpr int kWords = kRun / 2;
+  // The unit runs in bfloat16 for every input type (binary16 coefficients
+  // split into two bfloat16 words each, see above).
+  constexpr bool kF16 = DT == TCU_F16_F32;
+  constexpr int UDT = TCU_BF16_F32;
 
   const int lane = threadIdx.x & 63;
   const int r = lane & 15, g = lane >> 4;
@@ -130,7 +135,7 @@ __global__ __launch_bounds__(kPolyThreads) void poly_kernel(const unsigned char 
 #pragma unroll
       for (int q = 0; q < kWords; ++q) {
         unsigned hi, lo;
-        split2<DT>(pw[2 * q], pw[2 * q + 1], hi, lo);
+        split_bf16(pw[2 * q], pw[2 * q + 1], hi, lo);
         xh[u][q] = hi;
         xl[u][q] = lo;
       }
@@ -175,8 +180,19 @@ __global__ __launch_bounds__(kPolyThreads) void poly_kernel(const unsigned char 
       }
     };
     for (int64_t J = nblocks - 1; J >= 0; --J) {
-      Run wf[kH];
+      Run wf[kH], wl[kH];
       load_block(J, wf);
+      if constexpr (kF16) {
+#pragma unroll
+        for (int h = 0; h < kH; ++h)
+#pragma unroll
+          for (int q = 0; q < kWords; ++q) {
+            unsigned hi, lo;
+            f16_pair_to_bf16(wf[h][q], hi, lo);
+            wf[h][q] = hi;
+            wl[h][q] = lo;
+          }
+      }
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         float t = 0.f;
@@ -184,11 +200,19 @@ __global__ __launch_bounds__(kPolyThreads) void poly_kernel(const unsigned char 
         for (int h = 0; h < kH; ++h) {
           f32x4 d;
           if constexpr (S == 32) {
-            d = mfma_k32(DT, wf[h], xh[u], f32x4{0.f, 0.f, 0.f, 0.f});
-            d = mfma_k32(DT, wf[h], xl[u], d);
+            d = mfma_k32(UDT, wf[h], xh[u], f32x4{0.f, 0.f, 0.f, 0.f});
+            d = mfma_k32(UDT, wf[h], xl[u], d);
+            if constexpr (kF16) {
+              d = mfma_k32(UDT, wl[h], xh[u], d);
+              d = mfma_k32(UDT, wl[h], xl[u], d);
+            }
           } else {
-            d = mfma_k16(DT, wf[h], xh[u], f32x4{0.f, 0.f, 0.f, 0.f});
-            d = mfma_k16(DT, wf[h], xl[u], d);
+            d = mfma_k16(UDT, wf[h], xh[u], f32x4{0.f, 0.f, 0.f, 0.f});
+            d = mfma_k16(UDT, wf[h], xl[u], d);
+            if constexpr (kF16) {
+              d = mfma_k16(UDT, wl[h], xh[u], d);
+              d = mfma_k16(UDT, wl[h], xl[u], d);
+            }
           }
           const float th = __builtin_fmaf(
               __builtin_fmaf(__builtin_fmaf(d[3], yv[u], d[2]), yv[u], d[1]), yv[u], d[0]);
@@ -218,7 +242,7 @@ __global__ __launch_bounds__(kPolyThreads) void poly_kernel(const unsigned char 
 template <int DT, int S>
 hipError_t launch_poly_one(const void *coef, int64_t n, const void *pts, int64_t np, void *out,
                            hipStream_t stream, int num_cus) {
-  constexpr int U = TCU_POLY_U;
+  constexpr int U = kPolyU;
   const int64_t nchunks = (np + 15) / 16;
   const int64_t nblocks = (n + (int64_t)S * S - 1) / ((int64_t)S * S);
   const int64_t want = (nchunks + 4 * U - 1) / (4 * U);

@@ -35,6 +35,7 @@ TCU_ERR_ALIGN = -4
 TCU_ERR_OVERLAP = -5
 TCU_ERR_HIP = -6
 TCU_ERR_NO_DEVICE = -7
+TCU_ERR_POINTER = -8
 
 TCU_F16_F32 = 0
 TCU_BF16_F32 = 1
@@ -42,6 +43,17 @@ TCU_BF16_BF16 = 2
 TCU_I8_I32 = 3
 
 TCU_ACCUMULATE = 1
+
+# Test overrides and the pointer-check switch (tcu_set_knob)
+TCU_KNOB_GEMM_KERNEL = 0
+TCU_KNOB_PP_GRID = 1
+TCU_KNOB_SPLIT_K = 2
+TCU_KNOB_TAIL_SPLIT = 3
+TCU_KNOB_CHECK_POINTERS = 4
+TCU_PATH_AUTO = 0
+TCU_PATH_FULL_TILE = 1
+TCU_PATH_GENERAL = 2
+TCU_PATH_RING = 3
 TCU_MAX_RECT_DIM = 1 << 30
 
 # Every symbol include/tcu.h declares: name -> (restype, argtypes)
@@ -71,6 +83,9 @@ SIGNATURES = {
     "tcu_work": (_i64, []),
     "tcu_reset_calls": (None, []),
     "tcu_strerror": (ctypes.c_char_p, [_int]),
+    "tcu_check_device_range": (_int, [_vp, _i64]),
+    "tcu_set_knob": (_int, [_int, _int]),
+    "tcu_get_knob": (_int, [_int]),
 }
 
 _lib = None
@@ -378,3 +393,18 @@ def tcu_reset_calls() -> None:
 
 def tcu_strerror(status: int) -> str:
     return lib().tcu_strerror(int(status)).decode()
+
+
+# ------------------------------------------- pointer checks, test overrides
+def tcu_check_device_range(ptr: int, nbytes: int) -> int:
+    """Status of the pointer check for [ptr, ptr + nbytes) (TCU_OK or a
+    negative code; returned, not raised)."""
+    return int(lib().tcu_check_device_range(ptr or None, int(nbytes)))
+
+
+def tcu_set_knob(knob: int, value: int) -> None:
+    _check(lib().tcu_set_knob(int(knob), int(value)), "tcu_set_knob")
+
+
+def tcu_get_knob(knob: int) -> int:
+    return int(lib().tcu_get_knob(int(knob)))

@@ -20,3 +20,19 @@ def oracle_mod():
     import oracle
     oracle._load()
     return oracle
+
+
+@pytest.fixture
+def knobs():
+    """Set test overrides of the library (tcu_set_knob) for one test; every
+    knob set is put back to 0 (the automatic choice) afterwards."""
+    from paper_1908_06649_amd import tcu
+    touched = []
+
+    def put(knob: int, value: int) -> None:
+        tcu.tcu_set_knob(knob, value)
+        touched.append(knob)
+
+    yield put
+    for k in touched:
+        tcu.tcu_set_knob(k, 0)

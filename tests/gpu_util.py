@@ -133,3 +133,8 @@ def run_rect(A: torch.Tensor, B: torch.Tensor, s: int, in_name: str, out: str,
         assert bool((outside == sent).all()), "wrote into C's row padding"
     assert guard_intact(buf, total), "wrote past the end of C"
     return to_np(C.contiguous())
+
+
+# Names of the product's kernel paths -> TCU_KNOB_GEMM_KERNEL values
+PATHS = {"auto": tcu.TCU_PATH_AUTO, "fast": tcu.TCU_PATH_FULL_TILE,
+         "general": tcu.TCU_PATH_GENERAL, "ring": tcu.TCU_PATH_RING}

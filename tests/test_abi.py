@@ -56,7 +56,7 @@ def test_library_exports_every_declared_symbol(L):
 
 
 def test_strerror_covers_all_codes(L):
-    for code in range(0, -8, -1):
+    for code in range(0, -9, -1):
         msg = tcu.tcu_strerror(code)
         assert msg and "unknown" not in msg
     assert "unknown" in tcu.tcu_strerror(-99)
@@ -73,6 +73,46 @@ def test_unit_and_dtype_config(L):
     assert L.tcu_set_dtype(tcu.TCU_F16_F32) == tcu.TCU_OK
     assert L.tcu_set_stream(0x1234) == tcu.TCU_OK and L.tcu_get_stream() == 0x1234
     assert L.tcu_set_stream(None) == tcu.TCU_OK and not L.tcu_get_stream()
+
+
+def test_knobs_set_get_and_reject(L):
+    """Test overrides: set, read back, reset; unknown knobs and values out of
+    range are rejected and leave the knob unchanged."""
+    for knob, good in ((tcu.TCU_KNOB_GEMM_KERNEL, tcu.TCU_PATH_RING), (tcu.TCU_KNOB_PP_GRID, 3),
+                       (tcu.TCU_KNOB_SPLIT_K, 4), (tcu.TCU_KNOB_TAIL_SPLIT, 1),
+                       (tcu.TCU_KNOB_CHECK_POINTERS, 1)):
+        start = L.tcu_get_knob(knob)
+        assert L.tcu_set_knob(knob, good) == tcu.TCU_OK and L.tcu_get_knob(knob) == good
+        assert L.tcu_set_knob(knob, -1) == tcu.TCU_ERR_UNSUPPORTED
+        assert L.tcu_get_knob(knob) == good
+        assert L.tcu_set_knob(knob, start) == tcu.TCU_OK
+    assert L.tcu_set_knob(tcu.TCU_KNOB_GEMM_KERNEL, 4) == tcu.TCU_ERR_UNSUPPORTED
+    assert L.tcu_set_knob(tcu.TCU_KNOB_CHECK_POINTERS, 2) == tcu.TCU_ERR_UNSUPPORTED
+    assert L.tcu_set_knob(5, 0) == tcu.TCU_ERR_UNSUPPORTED
+    assert L.tcu_set_knob(-1, 0) == tcu.TCU_ERR_UNSUPPORTED
+    assert L.tcu_get_knob(5) == -1 and L.tcu_get_knob(-1) == -1
+
+
+def test_debug_env_turns_pointer_checks_on():
+    """TCU_DEBUG at load time sets the initial pointer-check knob (a fresh
+    process, since the environment is read once when the library loads)."""
+    code = ("from paper_1908_06649_amd import tcu; "
+            "print(tcu.tcu_get_knob(tcu.TCU_KNOB_CHECK_POINTERS))")
+    for env_val, want in (("1", "1"), ("0", "0"), (None, "0")):
+        env = dict(os.environ)
+        env.pop("TCU_DEBUG", None)
+        if env_val is not None:
+            env["TCU_DEBUG"] = env_val
+        out = subprocess.run([os.sys.executable, "-c", code], cwd=ROOT, env=env,
+                             capture_output=True, text=True, check=True).stdout.strip()
+        assert out.splitlines()[-1] == want, (env_val, out)
+
+
+def test_check_device_range_arguments(L):
+    assert L.tcu_check_device_range(PA, 0) == tcu.TCU_OK        # empty range: nothing to check
+    assert L.tcu_check_device_range(PA, -1) == tcu.TCU_ERR_SHAPE
+    if not torch.cuda.is_available():
+        assert L.tcu_check_device_range(PA, 16) == tcu.TCU_ERR_NO_DEVICE
 
 
 def test_config_is_per_thread(L):
@@ -431,3 +471,4 @@ def test_new_entry_points_valid_arguments_without_device(L):
     assert L.tcu_transitive_closure_ex(PA, 64, 64, 32, None) == tcu.TCU_ERR_NO_DEVICE
     assert L.tcu_dft_ex(PA, PB, 0, 32, 4, 32, None) == tcu.TCU_ERR_NO_DEVICE
     assert L.tcu_dft_ex(PA, PB, PC, 1 << 20, 4, 32, None) == tcu.TCU_ERR_NO_DEVICE
+

@@ -61,3 +61,53 @@ def test_multi_gpu_request_exits_with_a_message():
                        capture_output=True, text=True, timeout=120)
     assert r.returncode != 0
     assert "one GPU" in r.stderr
+
+
+def test_model_time_is_theorem2_form():
+    """T = a * work + calls * l with the fit of the workload's types and unit
+    size: for the product, a N^3/s + (N/s)^2 l."""
+    fits = {"bf16_f32_s32": {"a_s_per_work": 2e-12, "ell_us": 4.0}}
+    sp = inputs.WORKLOADS["gemm_bf16_N8192_s32"]
+    N, s = 8192, 32
+    mt = bench.model_time(sp, (N // s) ** 2, N ** 3 // s, 0.8, fits)
+    want = 2e-12 * N ** 3 / s + (N // s) ** 2 * 4e-6
+    assert abs(mt["T_model_ms"] - want * 1e3) <= 1e-9 * want * 1e3
+    assert abs(mt["measured_over_model"] - 0.8e-3 / want) < 1e-12
+    assert bench.model_time(inputs.WORKLOADS["gemm_i8_N8192_s32"], 1, 1, 1.0, fits) is None
+
+
+class _FakeWorkload:
+    """A measured workload whose 'GPU result' is the oracle's own, rounded to
+    the output type: the baseline's sampling and parity logic must accept it."""
+
+    def __init__(self, name, perturb=0.0):
+        import numpy as np
+        import torch
+        import oracle
+        self.spec = dict(inputs.WORKLOADS[name])
+        self.A, self.B = inputs.make_inputs(self.spec)
+        ref = oracle.mm(inputs.bits(self.A), inputs.bits(self.B), self.spec["dtype"])
+        if self.spec["out"] == "i32":
+            self.C = torch.from_numpy(ref.astype(np.int32))
+        elif self.spec["out"] == "bf16":
+            self.C = torch.from_numpy(oracle.f64_to_bf16(ref).view(np.int16)).view(torch.bfloat16)
+        else:
+            self.C = torch.from_numpy((ref * (1 + perturb)).astype(np.float32))
+
+
+@pytest.mark.parametrize("name", ["tall_f16_n4096_s16", "gemm_f16_N1024_s16"])
+def test_cpu_baseline_logic(name):
+    rep = bench.cpu_baseline(_FakeWorkload(name), target_s=2.0)
+    assert rep["kind"] == "oracle" and rep["cores"] >= 1 and rep["seconds"] > 0
+    assert "output rows" in rep["sample"]
+
+
+def test_cpu_baseline_rejects_a_wrong_result():
+    with pytest.raises(AssertionError):
+        bench.cpu_baseline(_FakeWorkload("gemm_f16_N1024_s16", perturb=0.01), target_s=2.0)
+
+
+def test_host_info_fields():
+    h = bench.host_info()
+    assert {"cpu_model", "nproc", "OMP_NUM_THREADS", "oracle_threads"} <= set(h)
+    assert h["nproc"] >= 1 and h["oracle_threads"] >= 1

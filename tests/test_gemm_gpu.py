@@ -7,7 +7,7 @@ import torch
 from oracle import compare, mm
 from paper_1908_06649_amd import inputs, tcu
 
-from gpu_util import DEV, draw_pair, run_gemm, run_tall, to_np
+from gpu_util import DEV, PATHS, draw_pair, run_gemm, run_tall, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -130,8 +130,8 @@ def test_workload_i8_N8192_s32_all_rows():
 @pytest.mark.parametrize("path", ["fast", "general", "ring"])
 @pytest.mark.parametrize("din,dout", DTYPES)
 @pytest.mark.parametrize("N,s", [(256, 16), (512, 32), (1280, 32)])
-def test_kernel_paths(monkeypatch, path, din, dout, N, s):
-    monkeypatch.setenv("TCU_GEMM_KERNEL", path)
+def test_kernel_paths(knobs, path, din, dout, N, s):
+    knobs(tcu.TCU_KNOB_GEMM_KERNEL, PATHS[path])
     A, B = draw_pair((N, N), (N, N), din, seed=N + 3 * s)
     got = run_gemm(A, B, s, dout)
     compare.check(din, dout, inputs.bits(A), inputs.bits(B), got)
@@ -139,8 +139,8 @@ def test_kernel_paths(monkeypatch, path, din, dout, N, s):
 
 @pytest.mark.parametrize("path", ["fast", "general", "ring"])
 @pytest.mark.parametrize("din,dout", DTYPES)
-def test_kernel_paths_identity_permutation(monkeypatch, path, din, dout):
-    monkeypatch.setenv("TCU_GEMM_KERNEL", path)
+def test_kernel_paths_identity_permutation(knobs, path, din, dout):
+    knobs(tcu.TCU_KNOB_GEMM_KERNEL, PATHS[path])
     N, s = 768, 16
     A, _ = draw_pair((N, N), (N, N), din, seed=11)
     got = run_gemm(A, inputs.identity(N, din), s, dout)
@@ -151,8 +151,8 @@ def test_kernel_paths_identity_permutation(monkeypatch, path, din, dout):
 
 
 @pytest.mark.parametrize("path", ["fast", "general"])
-def test_kernel_paths_composition(monkeypatch, path):
-    monkeypatch.setenv("TCU_GEMM_KERNEL", path)
+def test_kernel_paths_composition(knobs, path):
+    knobs(tcu.TCU_KNOB_GEMM_KERNEL, PATHS[path])
     N, s = 256, 32
     A, B = draw_pair((N, N), (N, N), "i8", seed=13)
     full = run_gemm(A, B, s, "i32").astype(np.int64)

@@ -10,7 +10,7 @@ import numpy as np
 import pytest
 import torch
 
-from oracle import compare, poly_eval
+from oracle import bf16_to_f64, compare, poly_eval
 from paper_1908_06649_amd import inputs, tcu
 
 import gpu_util as gu
@@ -94,6 +94,35 @@ def test_poly_short_polynomial_large_points(s):
     compare.check_poly("bf16", "f32", inputs.bits(coef), inputs.bits(pts), got, s)
 
 
+@pytest.mark.parametrize("s", [16, 32])
+@pytest.mark.parametrize("din,out", PAIRS)
+def test_poly_sparse_high_powers_small_points(din, out, s):
+    """Only the highest power of a block nonzero (a_(s-1) = 1, and a_h for
+    h = -1 mod s in a longer polynomial), points with 0.1 <= |x| < 1: the
+    value is carried by x^(s-1) alone, far below binary16's normal range
+    (2^-14) for most points, yet every value must meet the bound relative to
+    sum_h |a_h||x|^h.  binary16 X words would lose these terms entirely."""
+    g = torch.Generator().manual_seed(41 + s)
+    mag = 0.1 + 0.9 * torch.rand(3000, generator=g)
+    sign = torch.where(torch.rand(3000, generator=g) < 0.5, -1.0, 1.0)
+    pts = (mag * sign).to(inputs.TORCH_DTYPE[din])
+    for n in (s, 3 * s * s):
+        coef = torch.zeros(n)
+        coef[s - 1::s] = 1.0
+        coef = coef.to(inputs.TORCH_DTYPE[din])
+        got = run_poly(coef, pts, s, out)
+        rep = compare.check_poly(din, out, inputs.bits(coef), inputs.bits(pts), got, s)
+        print(din, out, s, n, rep)
+    # the advisor's example: a_31 = 1 at x = 0.5 is exactly 2^-31
+    coef = torch.zeros(s)
+    coef[s - 1] = 1.0
+    got = run_poly(coef.to(inputs.TORCH_DTYPE[din]),
+                   torch.tensor([0.5, -0.5, 0.25]).to(inputs.TORCH_DTYPE[din]), s, out)
+    want = np.array([0.5, -0.5, 0.25]) ** (s - 1)
+    val = bf16_to_f64(got) if out == "bf16" else np.asarray(got, dtype=np.float64)
+    assert np.all(np.abs(val - want) <= 2.0 ** -8 * np.abs(want)), (val, want)
+
+
 @pytest.mark.parametrize("din,out", PAIRS)
 def test_poly_no_coefficients_gives_zeros(din, out):
     pts = torch.linspace(-1, 1, 50).to(inputs.TORCH_DTYPE[din])
@@ -111,12 +140,15 @@ def test_poly_no_points_is_a_noop():
 
 
 @pytest.mark.parametrize("s", [16, 32])
-def test_poly_call_accounting(s):
+@pytest.mark.parametrize("din,per_block", [("bf16", 2), ("f16", 4)])
+def test_poly_call_accounting(s, din, per_block):
+    """Each of the n/m calls is issued for X_hi and X_lo, and for binary16
+    coefficients also for c_hi and c_lo."""
     n, p = 5000, 700
-    coef, pts = draw(n, p, "bf16", 3)
+    coef, pts = draw(n, p, din, 3)
     tcu.tcu_reset_calls()
     run_poly(coef, pts, s, "f32")
-    calls = 2 * -(-n // (s * s))
+    calls = per_block * -(-n // (s * s))
     assert tcu.tcu_calls() == calls
     assert tcu.tcu_square_calls() == calls * -(-p // s)
 

@@ -74,10 +74,10 @@ FULL = [(256, 32, 256), (256, 64, 512), (512, 1024, 768), (768, 2048, 256)]
 @pytest.mark.parametrize("accumulate", [False, True])
 @pytest.mark.parametrize("din,out", PAIRS)
 @pytest.mark.parametrize("M,K,N", FULL)
-def test_rect_full_tiles(M, K, N, din, out, accumulate, kernel, monkeypatch):
+def test_rect_full_tiles(M, K, N, din, out, accumulate, kernel, knobs):
     if din == "i8" and K % 64:
         K = 64 * ((K + 63) // 64)
-    monkeypatch.setenv("TCU_GEMM_KERNEL", kernel)
+    knobs(tcu.TCU_KNOB_GEMM_KERNEL, gu.PATHS[kernel])
     run_and_check(M, K, N, din, out, 32, "padded", accumulate, seed=M + K + N)
 
 
@@ -92,8 +92,8 @@ RING = [(64, 64, 64), (64, 128, 192), (192, 448, 128), (320, 960, 128), (128, 40
 @pytest.mark.parametrize("accumulate", [False, True])
 @pytest.mark.parametrize("din,out", PAIRS[:3])
 @pytest.mark.parametrize("M,K,N", RING)
-def test_rect_ring_kernel(M, K, N, din, out, accumulate, pitch, monkeypatch):
-    monkeypatch.setenv("TCU_GEMM_KERNEL", "ring")
+def test_rect_ring_kernel(M, K, N, din, out, accumulate, pitch, knobs):
+    knobs(tcu.TCU_KNOB_GEMM_KERNEL, tcu.TCU_PATH_RING)
     s = 32 if din == "bf16" else 16
     run_and_check(M, K, N, din, out, s, pitch, accumulate, seed=M + 5 * K + 11 * N)
 
@@ -132,36 +132,36 @@ def test_rect_large_ragged_padded_pitches(din, out, accumulate, N):
 
 @pytest.mark.parametrize("din,out", PAIRS)
 @pytest.mark.parametrize("accumulate", [False, True])
-def test_rect_full_tiles_many_per_workgroup(din, out, accumulate, monkeypatch):
+def test_rect_full_tiles_many_per_workgroup(din, out, accumulate, knobs):
     """The full-tile kernel's persistent loop with 3 workgroups for 12 tiles
     of 256 x 256 (each workgroup walks 4 tiles, reloading its ring)."""
-    monkeypatch.setenv("TCU_GEMM_KERNEL", "fast")
-    monkeypatch.setenv("TCU_PP_GRID", "3")
+    knobs(tcu.TCU_KNOB_GEMM_KERNEL, tcu.TCU_PATH_FULL_TILE)
+    knobs(tcu.TCU_KNOB_PP_GRID, 3)
     run_and_check(768, 512, 1024, din, out, 32, "padded", accumulate, seed=12)
 
 
 @pytest.mark.parametrize("nsplit", [2, 3, 4, 7])
 @pytest.mark.parametrize("din,out", PAIRS)
 @pytest.mark.parametrize("accumulate", [False, True])
-def test_rect_split_k(din, out, accumulate, nsplit, monkeypatch):
+def test_rect_split_k(din, out, accumulate, nsplit, knobs):
     """Split-K on the full-tile kernel: the stages cut into nsplit ranges
     whose partial tiles are added into C atomically (after zeroing C when
     overwriting).  int32 stays bit-exact; a bfloat16 output is never split
     (rounded once), so it must pass the single-rounding check."""
-    monkeypatch.setenv("TCU_GEMM_KERNEL", "fast")
-    monkeypatch.setenv("TCU_SPLIT_K", str(nsplit))
+    knobs(tcu.TCU_KNOB_GEMM_KERNEL, tcu.TCU_PATH_FULL_TILE)
+    knobs(tcu.TCU_KNOB_SPLIT_K, nsplit)
     run_and_check(512, 1344 if din != "i8" else 2688, 256, din, out, 32, "padded", accumulate,
                   seed=40 + nsplit)
 
 
 @pytest.mark.parametrize("din,out", PAIRS)
-def test_rect_split_k_many_items_per_workgroup(din, out, monkeypatch):
+def test_rect_split_k_many_items_per_workgroup(din, out, knobs):
     """Split-K items walked by a persistent grid of 5 workgroups: 6 tiles
     x 3 K ranges = 18 items, the first 16 in the permuted (XCD-grouped)
     order and the last 2 in their own."""
-    monkeypatch.setenv("TCU_GEMM_KERNEL", "fast")
-    monkeypatch.setenv("TCU_PP_GRID", "5")
-    monkeypatch.setenv("TCU_SPLIT_K", "3")
+    knobs(tcu.TCU_KNOB_GEMM_KERNEL, tcu.TCU_PATH_FULL_TILE)
+    knobs(tcu.TCU_KNOB_PP_GRID, 5)
+    knobs(tcu.TCU_KNOB_SPLIT_K, 3)
     run_and_check(512, 768 if din != "i8" else 1536, 768, din, out, 32, "padded", True,
                   seed=61)
 
@@ -174,32 +174,32 @@ def test_rect_split_k_many_items_per_workgroup(din, out, monkeypatch):
 @pytest.mark.parametrize("M,N,grid,ns", [(512, 1280, 4, 3), (768, 1024, 8, 4)])
 @pytest.mark.parametrize("din,out", PAIRS)
 @pytest.mark.parametrize("accumulate", [False, True])
-def test_rect_tail_split(M, N, grid, ns, din, out, accumulate, monkeypatch):
-    monkeypatch.setenv("TCU_GEMM_KERNEL", "fast")
-    monkeypatch.setenv("TCU_PP_GRID", str(grid))
-    monkeypatch.setenv("TCU_TAIL_SPLIT", str(ns))
+def test_rect_tail_split(M, N, grid, ns, din, out, accumulate, knobs):
+    knobs(tcu.TCU_KNOB_GEMM_KERNEL, tcu.TCU_PATH_FULL_TILE)
+    knobs(tcu.TCU_KNOB_PP_GRID, grid)
+    knobs(tcu.TCU_KNOB_TAIL_SPLIT, ns)
     K = 31 * 64 // ES[din]                  # 31 stages: uneven ranges
     run_and_check(M, K, N, din, out, 32, "padded", accumulate, seed=M + N + ns)
 
 
 @pytest.mark.parametrize("din,out", PAIRS)
-def test_rect_tail_split_chosen_by_size(din, out, monkeypatch):
+def test_rect_tail_split_chosen_by_size(din, out, knobs):
     """Without forcing: 10 tiles on 4 workgroups and 64 stages give the 2
     tail tiles 2 ranges of 32 stages."""
-    monkeypatch.setenv("TCU_GEMM_KERNEL", "fast")
-    monkeypatch.setenv("TCU_PP_GRID", "4")
+    knobs(tcu.TCU_KNOB_GEMM_KERNEL, tcu.TCU_PATH_FULL_TILE)
+    knobs(tcu.TCU_KNOB_PP_GRID, 4)
     run_and_check(512, 64 * 64 // ES[din], 1280, din, out, 32, "padded", False, seed=5)
 
 
 @pytest.mark.parametrize("accumulate", [False, True])
 @pytest.mark.parametrize("din,out", PAIRS)
 @pytest.mark.parametrize("M,K,N", [(4101, 1000, 4176), (4375, 1000, 4104)])
-def test_rect_large_ragged_tail_split(M, K, N, din, out, accumulate, monkeypatch):
+def test_rect_large_ragged_tail_split(M, K, N, din, out, accumulate, knobs):
     """The ragged full-tile kernel with its tail tiles split 3 ways: edge
     tiles in the kernel (17 x 17 tiles) and, for int8 on the second shape,
     the 256-aligned interior (17 x 16 tiles) with the general kernel on the
     strips."""
-    monkeypatch.setenv("TCU_TAIL_SPLIT", "3")
+    knobs(tcu.TCU_KNOB_TAIL_SPLIT, 3)
     s = 32 if din == "bf16" else 16
     run_and_check(M, K, N, din, out, s, "contiguous", accumulate, seed=M + K + N + 1)
 
