@@ -69,8 +69,10 @@ typedef enum tcu_status {
     TCU_ERR_OVERLAP = -5,     /* C overlaps A or B */
     TCU_ERR_HIP = -6,         /* the HIP runtime reported an error (launch, device query) */
     TCU_ERR_NO_DEVICE = -7,   /* no HIP device is visible */
-    TCU_ERR_POINTER = -8      /* pointer checks on: an operand is not inside one device
+    TCU_ERR_POINTER = -8,     /* pointer checks on: an operand is not inside one device
                                  allocation of the current device (tcu_check_device_range) */
+    TCU_ERR_SCRATCH = -9      /* the problem needs more than the fixed scratch of an
+                                 allocation-free entry point (tcu_dft_noalloc) */
 } tcu_status;
 
 /* Element types (input, output) of the unit.  Floating-point inputs are
@@ -304,6 +306,28 @@ int tcu_transitive_closure_ex(void *X, int64_t n, int64_t ld, int s, void *hip_s
 int tcu_dft(const void *x, void *y, void *work, int64_t n, int64_t batch);
 int tcu_dft_ex(const void *x, void *y, void *work, int64_t n, int64_t batch, int s,
                void *hip_stream);
+
+/* ---- the DFT without a caller-supplied work buffer ----
+ *
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same
+ * transform as tcu_dft_ex, with the levels' second buffer taken from a
+ * fixed array of TCU_DFT_NOALLOC_MAX_BYTES bytes of device memory that the
+ * library holds on each device it runs on, from its first use there until
+ * the process ends.  The call itself allocates nothing.
+ *   x, y, n, batch, s, hip_stream: as tcu_dft_ex (y must not overlap x).
+ *   When the transform has more than one level (n > s), batch * n * 8 bytes
+ *   must not exceed TCU_DFT_NOALLOC_MAX_BYTES, else TCU_ERR_SCRATCH and
+ *   nothing is launched; one level needs no scratch and has no such limit.
+ * Every call on a device shares that device's array and leaves its
+ * contents behind (the levels overwrite it before reading it, so nothing is
+ * cleared): calls that overlap in time on one device -- on different
+ * streams, or from different host threads -- race on it and must be
+ * serialized by the caller.
+ * Errors: as tcu_dft_ex, plus TCU_ERR_SCRATCH.  Cost accounting: as tcu_dft. */
+#define TCU_DFT_NOALLOC_MAX_BYTES ((int64_t)64 << 20)
+int tcu_dft_noalloc(const void *x, void *y, int64_t n, int64_t batch, int s, void *hip_stream);
+
 /* ---- cost accounting (Theorem 2 proof; Section 5 weak model) ----
  * tcu_calls:        logical tensor-unit calls issued (1 per tall call,
  *                   (N/s)^2 per tcu_gemm).

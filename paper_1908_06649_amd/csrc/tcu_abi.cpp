@@ -479,6 +479,28 @@ TCU_EXPORT int tcu_dft(const void *x, void *y, void *work, int64_t n, int64_t ba
   return tcu_dft_ex(x, y, work, n, batch, g_cfg.s, g_cfg.stream);
 }
 
+TCU_EXPORT int tcu_dft_noalloc(const void *x, void *y, int64_t n, int64_t batch, int s,
+                               void *hip_stream) {
+  bool need_work = false;
+  int rc = validate_dft_xy(x, y, n, batch, s, &need_work);
+  if (rc != TCU_OK) return rc;
+  // the levels' second buffer is the library's fixed scratch array
+  if (need_work && batch * n * 8 > TCU_DFT_NOALLOC_MAX_BYTES) return TCU_ERR_SCRATCH;
+  if (batch == 0) return TCU_OK;
+  int num_cus = 0;
+  rc = device_ready(&num_cus);
+  if (rc != TCU_OK) return rc;
+  const int64_t bytes = batch * n * 8;
+  rc = check_ranges({{x, bytes}, {y, bytes}});
+  if (rc != TCU_OK) return rc;
+  if (tcu::launch_dft_noalloc(x, y, n, batch, s, (hipStream_t)hip_stream, num_cus) !=
+      hipSuccess)
+    return TCU_ERR_HIP;
+  count_dft(n, batch, s);
+  return TCU_OK;
+}
+
+
 TCU_EXPORT int64_t tcu_calls(void) { return g_calls.load(std::memory_order_relaxed); }
 TCU_EXPORT int64_t tcu_square_calls(void) { return g_square_calls.load(std::memory_order_relaxed); }
 TCU_EXPORT int64_t tcu_work(void) { return g_work.load(std::memory_order_relaxed); }
@@ -527,6 +549,8 @@ TCU_EXPORT const char *tcu_strerror(int status) {
     case TCU_ERR_HIP: return "HIP runtime error";
     case TCU_ERR_NO_DEVICE: return "no HIP device visible";
     case TCU_ERR_POINTER: return "an operand is not inside one device allocation of the current device";
+    case TCU_ERR_SCRATCH:
+      return "the problem exceeds the fixed scratch of the allocation-free entry point";
   }
   return "unknown tcu status";
 }

@@ -23,6 +23,8 @@
 // relative accuracy (one bf16 rounding would cost 2^-9 per level).  The
 // twiddles are computed in the kernel (sincospi of an exactly reduced
 // angle); nothing is precomputed or stored.
+#include <mutex>
+
 #include "tcu_device.h"
 #include "tcu_launch.h"
 
@@ -190,6 +192,11 @@ __global__ __launch_bounds__(kDftThreads) void dft_level_kernel(
   }
 }
 
+// Scratch of the allocation-free DFT (tcu_dft_noalloc): the levels' second
+// buffer.  In host code this name is only a stand-in for the symbol; the
+// array's device address comes from hipGetSymbolAddress, once per device.
+static __device__ __align__(256) unsigned char scratch[TCU_DFT_NOALLOC_MAX_BYTES];
+
 int ilog2(int64_t v) {
   int l = 0;
   while (((int64_t)1 << l) < v) ++l;
@@ -207,6 +214,29 @@ hipError_t launch_level(const f32x2 *src, f32x2 *dst, int64_t n, int R, int64_t 
   hipLaunchKernelGGL((dft_level_kernel<S>), dim3(blocks), dim3(kDftThreads), 0, stream, src, dst,
                      ilog2(n), ilog2(R), ilog2(P), ntrans);
   return hipGetLastError();
+}
+
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxScratchDevices] = {};
+
+// The scratch array's address on the current device (each device holds its
+// own copy), resolved with that device current on its first use there.
+hipError_t scratch_on_current_device(void **ptr) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxScratchDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return hipSuccess;
 }
 
 }  // namespace
@@ -234,6 +264,17 @@ hipError_t launch_dft(const void *x, void *y, void *work, int64_t n, int64_t bat
     P *= R;
   }
   return hipSuccess;
+}
+
+hipError_t launch_dft_noalloc(const void *x, void *y, int64_t n, int64_t batch, int s,
+                              hipStream_t stream, int num_cus) {
+  if (n <= 0 || batch <= 0) return hipSuccess;
+  void *work = nullptr;
+  if (dft_levels(n, s) > 1) {
+    const hipError_t e = scratch_on_current_device(&work);
+    if (e != hipSuccess) return e;
+  }
+  return launch_dft(x, y, work, n, batch, s, stream, num_cus);
 }
 
 }  // namespace tcu

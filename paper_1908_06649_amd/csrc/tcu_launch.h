@@ -67,6 +67,11 @@ hipError_t launch_tc_tiles(unsigned char *X, int64_t ld, int n, int k0, int tile
 int dft_levels(int64_t n, int s);
 hipError_t launch_dft(const void *x, void *y, void *work, int64_t n, int64_t batch, int s,
                       hipStream_t stream, int num_cus);
+// The same with the levels' second buffer in the library's fixed device
+// array (TCU_DFT_NOALLOC_MAX_BYTES; the caller has checked the size); its
+// address on the current device is resolved once per device.
+hipError_t launch_dft_noalloc(const void *x, void *y, int64_t n, int64_t batch, int s,
+                              hipStream_t stream, int num_cus);
 
 // Batch polynomial evaluation: out[i] = sum_{h<n} coef[h] * pts[i]^h for
 // i < np, 16-bit inputs (dtype TCU_F16_F32, TCU_BF16_F32 or TCU_BF16_BF16).

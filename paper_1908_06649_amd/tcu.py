@@ -36,6 +36,7 @@ TCU_ERR_OVERLAP = -5
 TCU_ERR_HIP = -6
 TCU_ERR_NO_DEVICE = -7
 TCU_ERR_POINTER = -8
+TCU_ERR_SCRATCH = -9
 
 TCU_F16_F32 = 0
 TCU_BF16_F32 = 1
@@ -78,6 +79,7 @@ SIGNATURES = {
     "tcu_transitive_closure_ex": (_int, [_vp, _i64, _i64, _int, _vp]),
     "tcu_dft": (_int, [_vp, _vp, _vp, _i64, _i64]),
     "tcu_dft_ex": (_int, [_vp, _vp, _vp, _i64, _i64, _int, _vp]),
+    "tcu_dft_noalloc": (_int, [_vp, _vp, _i64, _i64, _int, _vp]),
     "tcu_calls": (_i64, []),
     "tcu_square_calls": (_i64, []),
     "tcu_work": (_i64, []),
@@ -372,6 +374,18 @@ def tcu_dft_ex(x, y, work, n: int, batch: int, s: int, stream_ptr: int | None = 
     dev, px, py, pw = _dft_args("tcu_dft_ex", x, y, work, n, batch)
     st = _stream_ptr(dev) if stream_ptr is None else stream_ptr
     _check(lib().tcu_dft_ex(px, py, pw, int(n), int(batch), int(s), st), "tcu_dft_ex")
+
+
+TCU_DFT_NOALLOC_MAX_BYTES = 64 << 20
+
+
+def tcu_dft_noalloc(x, y, n: int, batch: int, s: int, stream_ptr: int | None = None) -> None:
+    """The DFT with the levels' second buffer in the library's fixed device
+    scratch (no allocation; batch * n * 8 <= TCU_DFT_NOALLOC_MAX_BYTES when
+    n > s); calls overlapping in time on one device race on that scratch."""
+    dev, px, py, _ = _dft_args("tcu_dft_noalloc", x, y, None, n, batch)
+    st = _stream_ptr(dev) if stream_ptr is None else stream_ptr
+    _check(lib().tcu_dft_noalloc(px, py, int(n), int(batch), int(s), st), "tcu_dft_noalloc")
 
 
 # --------------------------------------------------------- cost accounting

@@ -56,7 +56,7 @@ def test_library_exports_every_declared_symbol(L):
 
 
 def test_strerror_covers_all_codes(L):
-    for code in range(0, -9, -1):
+    for code in range(0, -10, -1):
         msg = tcu.tcu_strerror(code)
         assert msg and "unknown" not in msg
     assert "unknown" in tcu.tcu_strerror(-99)
@@ -472,3 +472,32 @@ def test_new_entry_points_valid_arguments_without_device(L):
     assert L.tcu_dft_ex(PA, PB, 0, 32, 4, 32, None) == tcu.TCU_ERR_NO_DEVICE
     assert L.tcu_dft_ex(PA, PB, PC, 1 << 20, 4, 32, None) == tcu.TCU_ERR_NO_DEVICE
 
+
+NOALLOC_ERRORS = [
+    # (x, y, n, batch, s) -> status; the levels' second buffer is the library's
+    ((PA, PB, 1024, 1, 8), tcu.TCU_ERR_UNSUPPORTED),
+    ((PA, PB, 96, 1, 32), tcu.TCU_ERR_SHAPE),
+    ((0, PB, 1024, 1, 32), tcu.TCU_ERR_NULL),
+    ((PA, PB + 8, 1024, 1, 32), tcu.TCU_ERR_ALIGN),
+    ((PA, PA + 4096, 1024, 1, 32), tcu.TCU_ERR_OVERLAP),
+    # two levels: batch * n * 8 bytes above the fixed scratch
+    ((PA, PC, 1 << 20, 9, 32), tcu.TCU_ERR_SCRATCH),
+    ((PA, PC, 1 << 24, 1, 32), tcu.TCU_ERR_SCRATCH),
+]
+
+
+@pytest.mark.parametrize("args,want", NOALLOC_ERRORS)
+def test_dft_noalloc_rejects(L, args, want):
+    L.tcu_reset_calls()
+    assert L.tcu_dft_noalloc(*args, None) == want
+    assert L.tcu_calls() == 0
+
+
+@pytest.mark.skipif(torch.cuda.device_count() > 0, reason="a HIP device is visible")
+def test_dft_noalloc_limits_without_device(L):
+    """At the scratch limit, and a one-level transform of any size (no
+    scratch needed), the call gets as far as the device check."""
+    assert tcu.TCU_DFT_NOALLOC_MAX_BYTES == 64 << 20
+    assert L.tcu_dft_noalloc(PA, 0x4000000000, 1 << 20, 8, 32, None) == tcu.TCU_ERR_NO_DEVICE
+    assert L.tcu_dft_noalloc(PA, 0x4000000000, 32, 1 << 24, 32, None) == tcu.TCU_ERR_NO_DEVICE
+    assert L.tcu_dft_noalloc(0, 0, 1024, 0, 32, None) == tcu.TCU_OK
