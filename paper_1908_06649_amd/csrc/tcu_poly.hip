@@ -43,6 +43,7 @@ namespace {
 
 constexpr int kPolyThreads = 256;  // 4 waves per workgroup
 constexpr int kPolyU = 4;          // 16-point chunks per wave and pass
+constexpr int kPolyLongBlocks = 8; // coefficient blocks from which a pass takes 2 kPolyU chunks
 
 template <int DT>
 __device__ __forceinline__ float in_to_f32(unsigned bits16) {
@@ -239,10 +240,9 @@ __global__ __launch_bounds__(kPolyThreads) void poly_kernel(const unsigned char 
   }
 }
 
-template <int DT, int S>
-hipError_t launch_poly_one(const void *coef, int64_t n, const void *pts, int64_t np, void *out,
-                           hipStream_t stream, int num_cus) {
-  constexpr int U = kPolyU;
+template <int DT, int S, int U>
+hipError_t launch_poly_u(const void *coef, int64_t n, const void *pts, int64_t np, void *out,
+                         hipStream_t stream, int num_cus) {
   const int64_t nchunks = (np + 15) / 16;
   const int64_t nblocks = (n + (int64_t)S * S - 1) / ((int64_t)S * S);
   const int64_t want = (nchunks + 4 * U - 1) / (4 * U);
@@ -252,6 +252,18 @@ hipError_t launch_poly_one(const void *coef, int64_t n, const void *pts, int64_t
                      (const unsigned char *)coef, n, (const unsigned char *)pts, np,
                      (unsigned char *)out, nchunks, nblocks);
   return hipGetLastError();
+}
+
+// Each pass of a wave loads every coefficient block once for its U chunks
+// of 16 points: long polynomials (8 or more blocks) take 8 chunks per pass,
+// halving the coefficient traffic per point.
+template <int DT, int S>
+hipError_t launch_poly_one(const void *coef, int64_t n, const void *pts, int64_t np, void *out,
+                           hipStream_t stream, int num_cus) {
+  const int64_t nblocks = (n + (int64_t)S * S - 1) / ((int64_t)S * S);
+  if (nblocks >= kPolyLongBlocks)
+    return launch_poly_u<DT, S, 2 * kPolyU>(coef, n, pts, np, out, stream, num_cus);
+  return launch_poly_u<DT, S, kPolyU>(coef, n, pts, np, out, stream, num_cus);
 }
 
 }  // namespace

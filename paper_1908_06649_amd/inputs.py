@@ -53,6 +53,10 @@ RECT_WORKLOADS = {
 POLY_WORKLOADS = {
     "poly_bf16_n4096_p16777216_s32": dict(kind="poly", dtype="bf16", out="f32", n=4096,
                                           p=1 << 24, s=32, seed=8),
+    # a long polynomial: n/m = 64 unit calls per point, where the theorem's
+    # matrix term n p / sqrt(m) dominates its scalar terms
+    "poly_bf16_n65536_p4194304_s32": dict(kind="poly", dtype="bf16", out="f32", n=1 << 16,
+                                          p=1 << 22, s=32, seed=11),
 }
 
 # Workloads of the transitive closure (tcu_transitive_closure, Theorem 5):
