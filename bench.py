@@ -47,7 +47,7 @@ Timing: every measured call first runs back to back, untimed, for 0.3 s
 calls bracketed by HIP events on the stream the library launches on.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
-       [--no-cpu-baseline] [--no-secondary] [--copy-probe]
+       [--no-cpu-baseline] [--no-secondary] [--copy-probe] [--mfma-probe]
 """
 from __future__ import annotations
 
@@ -536,6 +536,65 @@ def copy_probe() -> None:
                       "GB_per_s_read_plus_write": 2 * nbytes / (ms * 1e-3) / 1e9}))
 
 
+def mfma_probe(iters: int = 100000, reps: int = 3) -> None:
+    """The matrix cores' sustained rate on this chip with nothing else
+    running (libtcu_probe.so: the product's persistent grid, one workgroup of
+    8 waves per CU, each wave issuing the product's 32-instruction phase from
+    registers `iters` times), for bfloat16 and int8 operands drawn at random
+    as in the workloads and for constant operands: the power-limited ceiling
+    the products are measured against.  Prints one JSON line."""
+    import ctypes
+    import torch
+    from paper_1908_06649_amd import build as hip_build
+    from paper_1908_06649_amd import tcu
+    lib = ctypes.CDLL(hip_build.PROBE_LIB)
+    fn = lib.tcu_probe_mfma
+    fn.restype = ctypes.c_int
+    fn.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int,
+                   ctypes.c_void_p]
+    blocks = torch.cuda.get_device_properties(0).multi_processor_count
+    words = blocks * 512 * 12 * 4                 # 12 16-byte operands per lane
+    g = torch.Generator(device="cuda").manual_seed(77)
+    out = torch.empty(blocks * 512, dtype=torch.int32, device="cuda")
+    res = {"probe": "matrix-core ceiling", "blocks": blocks, "waves_per_block": 8,
+           "instructions_per_wave": 32 * iters}
+    st = torch.cuda.current_stream()
+    for name, dt, peak in (("bf16", tcu.TCU_BF16_F32, PEAK["bf16"]),
+                           ("i8", tcu.TCU_I8_I32, PEAK["i8"])):
+        for kind in ("random", "constant"):
+            if kind == "constant":
+                ops = torch.full((words,), 0x3F803F80 if name == "bf16" else 0x01010101,
+                                 dtype=torch.int32, device="cuda")
+            elif name == "bf16":
+                ops = torch.randn(words * 2, generator=g, device="cuda").to(torch.bfloat16)
+                ops = ops.view(torch.int32)
+            else:
+                ops = torch.randint(-128, 128, (words * 4,), generator=g, device="cuda",
+                                    dtype=torch.int8).view(torch.int32)
+            assert ops.numel() == words and out.numel() == blocks * 512
+
+            def run():
+                rc = fn(dt, ops.data_ptr(), out.data_ptr(), iters, blocks, st.cuda_stream)
+                if rc != 0:
+                    raise RuntimeError(f"probe launch failed ({rc})")
+
+            run()
+            torch.cuda.synchronize()
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(st)
+            for _ in range(reps):
+                run()
+            e1.record(st)
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / reps
+            flops = blocks * 8 * 32 * iters * (16 * 16 * 32 * 2 if name == "bf16" else
+                                               16 * 16 * 64 * 2)
+            rate = flops / (ms * 1e-3) / 1e12
+            res[f"{name}_{kind}"] = {"ms": ms, "T_per_s": rate, "frac_of_peak": rate / peak}
+    print(json.dumps(res), flush=True)
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -549,6 +608,7 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--copy-probe", action="store_true")
+    ap.add_argument("--mfma-probe", action="store_true")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -564,6 +624,9 @@ def main() -> int:
     tcu.lib()   # raises if the HIP library is missing: no fallback
     if args.copy_probe:
         copy_probe()
+        return 0
+    if args.mfma_probe:
+        mfma_probe()
         return 0
     known = {**inputs.WORKLOADS, **inputs.RECT_WORKLOADS, **inputs.POLY_WORKLOADS,
              **inputs.TC_WORKLOADS, **inputs.DFT_WORKLOADS}

@@ -16,6 +16,9 @@ LIB = os.path.join(HERE, "libtcu.so")
 # The benchmark's host-side timing loop (calls libtcu.so through the C ABI).
 TIMING_SRC = "tcu_timing.cpp"
 TIMING_LIB = os.path.join(HERE, "libtcu_timing.so")
+# The benchmark's matrix-core ceiling probe (a kernel of its own, outside the C ABI).
+PROBE_SRC = "tcu_probe.hip"
+PROBE_LIB = os.path.join(HERE, "libtcu_probe.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
 SOURCES = ["tcu_abi.cpp", "tcu_tall.hip", "tcu_gemm.hip", "tcu_poly.hip", "tcu_tc.hip",
            "tcu_dft.hip"]
@@ -70,6 +73,14 @@ def build(verbose: bool = False) -> str:
     if res.returncode != 0:
         raise RuntimeError(f"hipcc failed for {TIMING_SRC}:\n{res.stdout}\n{res.stderr}")
     os.replace(tmp, TIMING_LIB)
+    tmp = PROBE_LIB + ".tmp"
+    cmd = [hipcc(), *COMMON, "-shared", os.path.join(CSRC, PROBE_SRC), "-o", tmp]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        raise RuntimeError(f"hipcc failed for {PROBE_SRC}:\n{res.stdout}\n{res.stderr}")
+    os.replace(tmp, PROBE_LIB)
     return LIB
 
 
