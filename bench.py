@@ -76,7 +76,8 @@ PROFILES = os.path.join(ROOT, "profiles")
 
 def kernel_sources(kind: str):
     main = {"gemm": ["tcu_gemm.hip"], "rect": ["tcu_gemm.hip"], "poly": ["tcu_poly.hip"],
-            "tc": ["tcu_tc.hip", "tcu_gemm.hip"], "dft": ["tcu_dft.hip"]}.get(kind, ["tcu_tall.hip"])
+            "tc": ["tcu_tc.hip", "tcu_gemm.hip"], "dft": ["tcu_dft.hip"],
+            "probe": ["tcu_probe.hip"]}.get(kind, ["tcu_tall.hip"])
     return [os.path.join(CSRC, f) for f in (*main, "tcu_device.h")]
 
 
