@@ -134,8 +134,12 @@ def poly_bound(dtype_in: str, n: int, s: int) -> float:
     (Theorem 11) as the unit computes it, times a safety factor of 4:
       * X = X_hi + X_lo as two bfloat16 words (for both input types; the
         binary16 coefficients are split exactly into two bfloat16 words)
-        leaves a residual of at most 2^-18 |x^k| (two nearest roundings of
-        9 significant bits);
+        leaves a residual of at most 2^-17 |x^k|: hi is x^k rounded to
+        nearest with 8 significant bits, so the remainder is at most 2^-8 of
+        the power of two 2^e at or below |x^k|, and strictly below it unless
+        it is exactly that power of two (then lo holds it exactly); a
+        remainder below 2^(e-8) rounds to 8 significant bits with an error of
+        at most 2^(e-17);
       * every power is a chain of at most 2 log2(s) + s binary32 products,
         the block weights y^(s J) a chain of n/s^2 more;
       * the unit's sums run over s products, the combine over s + n/s^2
@@ -144,7 +148,7 @@ def poly_bound(dtype_in: str, n: int, s: int) -> float:
     sum_h |a_h| |x|^h."""
     if dtype_in not in ("f16", "bf16"):
         raise ValueError("polynomial evaluation takes f16 or bf16 inputs")
-    split = 2.0 ** -18
+    split = 2.0 ** -17
     ops = 2 * 6 + s + s + 2 * (n // (s * s) + 1) + 8
     return 4.0 * (split + ops * 2.0 ** -24)
 
