@@ -75,8 +75,9 @@ PROFILES = os.path.join(ROOT, "profiles")
 
 
 def kernel_sources(kind: str):
-    main = {"gemm": ["tcu_gemm.hip"], "rect": ["tcu_gemm.hip"], "poly": ["tcu_poly.hip"],
-            "tc": ["tcu_tc.hip", "tcu_gemm.hip"], "dft": ["tcu_dft.hip"],
+    main = {"gemm": ["tcu_gemm.hip"], "rect": ["tcu_gemm.hip"],
+            "poly": ["tcu_poly.hip", "tcu_split.h"],
+            "tc": ["tcu_tc.hip", "tcu_gemm.hip"], "dft": ["tcu_dft.hip", "tcu_split.h"],
             "probe": ["tcu_probe.hip"]}.get(kind, ["tcu_tall.hip"])
     return [os.path.join(CSRC, f) for f in (*main, "tcu_device.h")]
 
@@ -593,7 +594,54 @@ def mfma_probe(iters: int = 100000, reps: int = 3) -> None:
                                                16 * 16 * 64 * 2)
             rate = flops / (ms * 1e-3) / 1e12
             res[f"{name}_{kind}"] = {"ms": ms, "T_per_s": rate, "frac_of_peak": rate / peak}
+    res["overlap"] = overlap_probe(lib, blocks, st)
     print(json.dumps(res), flush=True)
+
+
+def overlap_probe(lib, blocks: int, st, iters: int = 10000, reps: int = 3) -> dict:
+    """Whether binary32 vector FMAs run while the matrix core works
+    (libtcu_probe.so, tcu_probe_overlap; one workgroup of 8 waves per CU):
+    `same_wave` -- every wave issues 32 bfloat16 matrix-core instructions
+    per round, each followed by nv independent FMAs; `mfma_waves` /
+    `valu_waves` / `both` -- waves 0-3 issue only the 32 matrix-core
+    instructions per round, waves 4-7 (on the same SIMDs) only 32 nv FMAs,
+    each kind alone and both at once.  Milliseconds per launch of `iters`
+    rounds."""
+    import ctypes
+    import torch
+    fn = lib.tcu_probe_overlap
+    fn.restype = ctypes.c_int
+    fn.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                   ctypes.c_int, ctypes.c_void_p]
+    g = torch.Generator(device="cuda").manual_seed(78)
+    ops = torch.randn(blocks * 512 * 3 * 8, generator=g, device="cuda").to(torch.bfloat16)
+    ops = ops.view(torch.int32)
+    out = torch.empty(blocks * 512, dtype=torch.int32, device="cuda")
+    assert ops.numel() == blocks * 512 * 3 * 4
+
+    def timed(mode, nv):
+        def run():
+            rc = fn(mode, nv, ops.data_ptr(), out.data_ptr(), iters, blocks, st.cuda_stream)
+            if rc != 0:
+                raise RuntimeError(f"overlap probe launch failed ({rc})")
+        run()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(st)
+        for _ in range(reps):
+            run()
+        e1.record(st)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    res = {"iters": iters, "same_wave": {}, "separate_waves": {}}
+    for nv in (0, 1, 2, 3, 4, 6):
+        res["same_wave"][f"nv{nv}"] = timed(0, nv)
+    for nv in (2, 4, 6):
+        res["separate_waves"][f"nv{nv}"] = {"mfma_waves": timed(2, nv), "valu_waves": timed(3, nv),
+                                            "both": timed(1, nv)}
+    return res
 
 
 def main() -> int:

@@ -26,6 +26,7 @@
 #include <mutex>
 
 #include "tcu_device.h"
+#include "tcu_split.h"
 #include "tcu_launch.h"
 
 namespace tcu {
@@ -34,15 +35,6 @@ namespace {
 constexpr int kDftThreads = 256;
 
 typedef float f32x2 __attribute__((ext_vector_type(2)));
-
-// v = hi + lo as two bfloat16 (round to nearest even; the remainder v - hi is
-// exact in binary32), for a pair of values packed per word.
-__device__ __forceinline__ void split_pair(float v0, float v1, unsigned &hi, unsigned &lo) {
-  hi = pack_bf16x2(v0, v1);
-  const float h0 = __builtin_bit_cast(float, hi << 16);
-  const float h1 = __builtin_bit_cast(float, hi & 0xffff0000u);
-  lo = pack_bf16x2(v0 - h0, v1 - h1);
-}
 
 // exp(-2 pi i m / N) for 0 <= m < N, N a power of two: (cos, -sin) of pi x,
 // x = 2m/N formed exactly (N is a power of two).
@@ -82,6 +74,7 @@ __global__ __launch_bounds__(kDftThreads) void dft_level_kernel(
 
   const int lane = threadIdx.x & 63;
   const int r = lane & 15, g = lane >> 4;
+  const SplitConsts sc = split_consts();
 
   // Weights operand: row k = 16h + r, contracted run j = kRun g + e, value
   // w_R^(j k) (zero outside R x R), as hi/lo words; -Wi for the real part.
@@ -100,10 +93,10 @@ __global__ __launch_bounds__(kDftThreads) void dft_level_kernel(
 #pragma unroll
     for (int q = 0; q < kWords; ++q) {
       unsigned hi, lo;
-      split_pair(cr[2 * q], cr[2 * q + 1], hi, lo);
+      split_bf16x2(cr[2 * q], cr[2 * q + 1], hi, lo, sc);
       wr_h[h][q] = hi;
       wr_l[h][q] = lo;
-      split_pair(ci[2 * q], ci[2 * q + 1], hi, lo);
+      split_bf16x2(ci[2 * q], ci[2 * q + 1], hi, lo, sc);
       wi_h[h][q] = hi;
       wi_l[h][q] = lo;
       ni_h[h][q] = hi ^ 0x80008000u;   // -Wi: flip both signs
@@ -134,10 +127,10 @@ __global__ __launch_bounds__(kDftThreads) void dft_level_kernel(
 #pragma unroll
     for (int q = 0; q < kWords; ++q) {
       unsigned hi, lo;
-      split_pair(xr[2 * q], xr[2 * q + 1], hi, lo);
+      split_bf16x2(xr[2 * q], xr[2 * q + 1], hi, lo, sc);
       xr_h[q] = hi;
       xr_l[q] = lo;
-      split_pair(xi[2 * q], xi[2 * q + 1], hi, lo);
+      split_bf16x2(xi[2 * q], xi[2 * q + 1], hi, lo, sc);
       xi_h[q] = hi;
       xi_l[q] = lo;
     }

@@ -36,6 +36,7 @@
 // meaningful while |x|^(n-1) and the partial sums stay within binary32
 // range (the theorem assumes evaluation without overflow or underflow).
 #include "tcu_device.h"
+#include "tcu_split.h"
 #include "tcu_launch.h"
 
 namespace tcu {
@@ -53,23 +54,13 @@ __device__ __forceinline__ float in_to_f32(unsigned bits16) {
     return bf16_to_f32(bits16);
 }
 
-// Two binary32 values as the high ("hi") and remainder ("lo") bfloat16
-// words, packed two per 32-bit word: hi = v rounded to nearest even, lo =
-// (v - hi) rounded again (v - hi is exact in binary32), so hi + lo is v to
-// 2^-18 |v|, and exactly v when v has at most 16 significant bits.
-__device__ __forceinline__ void split_bf16(float v0, float v1, unsigned &hi, unsigned &lo) {
-  hi = pack_bf16x2(v0, v1);
-  const float h0 = __builtin_bit_cast(float, hi << 16);
-  const float h1 = __builtin_bit_cast(float, hi & 0xffff0000u);
-  lo = pack_bf16x2(v0 - h0, v1 - h1);
-}
-
 // A word of two binary16 coefficients as the exact sum of two words of
 // bfloat16 pairs (11 significant bits in 8 + 8).
-__device__ __forceinline__ void f16_pair_to_bf16(unsigned w, unsigned &hi, unsigned &lo) {
+__device__ __forceinline__ void f16_pair_to_bf16(unsigned w, unsigned &hi, unsigned &lo,
+                                                 SplitConsts sc) {
   const float f0 = (float)bitcast<_Float16>((unsigned short)(w & 0xffffu));
   const float f1 = (float)bitcast<_Float16>((unsigned short)(w >> 16));
-  split_bf16(f0, f1, hi, lo);
+  split_bf16x2(f0, f1, hi, lo, sc);
 }
 
 // b^(step * g) for lane group g = 0..3 from the ladder b^step, b^(2 step):
@@ -102,7 +93,12 @@ __global__ __launch_bounds__(kPolyThreads) void poly_kernel(const unsigned char 
 
   const int lane = threadIdx.x & 63;
   const int r = lane & 15, g = lane >> 4;
-  const int64_t wave = (int64_t)blockIdx.x * (kPolyThreads / 64) + (threadIdx.x >> 6);
+  const SplitConsts sc = split_consts();
+  // Wave-uniform chunk indices (readfirstlane: the compiler cannot prove
+  // threadIdx.x >> 6 uniform), so point addresses are a scalar base plus a
+  // per-lane 32-bit offset.
+  const int64_t wave = (int64_t)blockIdx.x * (kPolyThreads / 64) +
+                       __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int64_t nwaves = (int64_t)gridDim.x * (kPolyThreads / 64);
   const unsigned short *pt16 = (const unsigned short *)pts;
   const unsigned short *cf16 = (const unsigned short *)coef;
@@ -112,16 +108,24 @@ __global__ __launch_bounds__(kPolyThreads) void poly_kernel(const unsigned char 
     float yv[U], y16v[U], yg[U], acc[U], ystep[U];
     // All U points first (clamped index, then a select), so the loads are
     // in flight together.
+    // Points past np read as zero bits (+0 in both formats).
+    const int64_t p0 = t0 * 16;
+    const bool whole = p0 + 16 * U <= np;   // every point of the pass exists
+    const unsigned short *pp = pt16 + p0;
     unsigned short praw[U];
+    if (whole) {
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int64_t idx = (t0 + u) * 16 + r;
-      praw[u] = pt16[idx < np ? idx : np - 1];
+      for (int u = 0; u < U; ++u) praw[u] = pp[16 * u + r];
+    } else {
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int64_t idx = p0 + 16 * u + r;
+        praw[u] = idx < np ? pt16[idx] : (unsigned short)0;
+      }
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int64_t idx = (t0 + u) * 16 + r;
-      const float x = idx < np ? in_to_f32<DT>(praw[u]) : 0.f;
+      const float x = in_to_f32<DT>(praw[u]);
       // Power ladder (same products in every lane): x^2 .. x^16, y = x^S.
       const float x2 = x * x, x4 = x2 * x2, x8 = x4 * x4, x16 = x8 * x8;
       // X fragment: x^(kRun g + e), e < kRun, as hi + lo words.
@@ -136,7 +140,7 @@ __global__ __launch_bounds__(kPolyThreads) void poly_kernel(const unsigned char 
 #pragma unroll
       for (int q = 0; q < kWords; ++q) {
         unsigned hi, lo;
-        split_bf16(pw[2 * q], pw[2 * q + 1], hi, lo);
+        split_bf16x2(pw[2 * q], pw[2 * q + 1], hi, lo, sc);
         xh[u][q] = hi;
         xl[u][q] = lo;
       }
@@ -162,19 +166,20 @@ __global__ __launch_bounds__(kPolyThreads) void poly_kernel(const unsigned char 
     // coefficient array (a wave-uniform test) take plain vector loads.
     auto load_block = [&](int64_t J, Run (&wb)[kH]) __attribute__((always_inline)) {
       const bool full = (J + 1) * S * S <= n;
+      const unsigned short *cb = cf16 + J * S * S;   // wave-uniform block base
 #pragma unroll
       for (int h = 0; h < kH; ++h) {
-        const int64_t base = (J * S + 16 * h + r) * S + kRun * g;
+        const int off = (16 * h + r) * S + kRun * g;
         if (full) {
-          wb[h] = *(const Run *)(cf16 + base);
+          wb[h] = *(const Run *)(cb + off);
         } else {
-          const int64_t left = n - base;
+          const int64_t left = n - J * S * S - off;
           unsigned ww[kWords];
 #pragma unroll
           for (int q = 0; q < kWords; ++q) ww[q] = 0;
 #pragma unroll
           for (int e = 0; e < kRun; ++e)
-            if (e < left) ww[e >> 1] |= (unsigned)cf16[base + e] << (16 * (e & 1));
+            if (e < left) ww[e >> 1] |= (unsigned)cb[off + e] << (16 * (e & 1));
 #pragma unroll
           for (int q = 0; q < kWords; ++q) wb[h][q] = ww[q];
         }
@@ -189,7 +194,7 @@ __global__ __launch_bounds__(kPolyThreads) void poly_kernel(const unsigned char 
 #pragma unroll
           for (int q = 0; q < kWords; ++q) {
             unsigned hi, lo;
-            f16_pair_to_bf16(wf[h][q], hi, lo);
+            f16_pair_to_bf16(wf[h][q], hi, lo, sc);
             wf[h][q] = hi;
             wl[h][q] = lo;
           }
@@ -229,12 +234,12 @@ __global__ __launch_bounds__(kPolyThreads) void poly_kernel(const unsigned char 
       float v = acc[u] * yg[u];
       v += __shfl_xor(v, 16);
       v += __shfl_xor(v, 32);
-      const int64_t idx = (t0 + u) * 16 + r;
-      if (g == 0 && idx < np) {
+      if (g == 0 && (whole || p0 + 16 * u + r < np)) {
         if constexpr (DT == TCU_BF16_BF16)
-          ((unsigned short *)out)[idx] = (unsigned short)(pack_bf16x2(v, 0.f) & 0xffffu);
+          ((unsigned short *)out + p0)[16 * u + r] =
+              (unsigned short)(pack_bf16x2(v, 0.f) & 0xffffu);
         else
-          ((float *)out)[idx] = v;
+          ((float *)out + p0)[16 * u + r] = v;
       }
     }
   }

@@ -13,6 +13,10 @@
 // bounded by the matrix cores and the chip's clock under the power limit,
 // which depends on the operand values (the host passes random or constant
 // data).
+//
+// A second probe (tcu_probe_overlap) measures whether binary32 vector ALU
+// work runs while the matrix core works: interleaved in one wave's
+// instruction stream, or issued by other waves on the same SIMD.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -62,6 +66,78 @@ mfma_probe_kernel(const u32x4 *__restrict__ ops, int64_t iters, unsigned *__rest
   out[t] = h;
 }
 
+// Overlap probe: can binary32 vector ALU work run while the matrix core
+// works, and from which waves?  Every lane keeps 8 independent binary32
+// chains (v = v * c1 + c2) beside 8 independent bfloat16 accumulators.
+//   kMode 0 (one wave does both): each wave issues 32 matrix-core
+//     instructions per round, each followed by NV vector FMAs that do not
+//     depend on it (the order held by scheduling barriers);
+//   kMode 1 (separate waves): waves 0-3 issue the 32 matrix-core
+//     instructions per round, waves 4-7 -- on the same four SIMDs -- 32 * NV
+//     vector FMAs per round;
+//   kMode 2: only waves 0-3 (matrix core) work; kMode 3: only waves 4-7
+//     (vector ALU) work; the other waves write their word and exit.
+template <int kMode, int NV>
+__global__ __attribute__((amdgpu_flat_work_group_size(512, 512), amdgpu_waves_per_eu(2, 2))) void
+overlap_probe_kernel(const u32x4 *__restrict__ ops, int64_t iters, unsigned *__restrict__ out) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const bool mfma_wave = kMode == 0 || ((kMode == 1 || kMode == 2) && w < 4);
+  const bool valu_wave = kMode == 0 || ((kMode == 1 || kMode == 3) && w >= 4);
+  const u32x4 *p = ops + t * 3;
+  const u32x4 xw = p[0], ww = p[1], vw = p[2];
+  f32x4 acc[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float v[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) v[i] = __builtin_bit_cast(float, (vw[i & 3] >> (i & 4)) & 0x3f7fffffu);
+  const float c1 = 0.999f, c2 = 1e-3f;
+  if (mfma_wave && valu_wave) {
+    for (int64_t it = 0; it < iters; ++it) {
+#pragma unroll
+      for (int j = 0; j < 32; ++j) {
+        acc[j & 7] = mfma_k32(TCU_BF16_F32, ww, xw, acc[j & 7]);
+#pragma unroll
+        for (int i = 0; i < NV; ++i) v[(j * NV + i) & 7] = __builtin_fmaf(v[(j * NV + i) & 7], c1, c2);
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        if (NV > 0) __builtin_amdgcn_sched_group_barrier(0x002, NV, 0);
+      }
+    }
+  } else if (mfma_wave) {
+    for (int64_t it = 0; it < iters; ++it) {
+#pragma unroll
+      for (int j = 0; j < 32; ++j) acc[j & 7] = mfma_k32(TCU_BF16_F32, ww, xw, acc[j & 7]);
+    }
+  } else if (valu_wave) {
+    for (int64_t it = 0; it < iters; ++it) {
+#pragma unroll
+      for (int j = 0; j < 32 * NV; ++j) v[j & 7] = __builtin_fmaf(v[j & 7], c1, c2);
+    }
+  }
+  unsigned h = 0;
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+    h = h * 31u + __builtin_bit_cast(unsigned, acc[i][0] + acc[i][1] + acc[i][2] + acc[i][3] + v[i]);
+  out[t] = h;
+}
+
+template <int kMode>
+hipError_t launch_overlap(int nv, const u32x4 *ops, int64_t iters, unsigned *out, int blocks,
+                          hipStream_t stream) {
+  switch (nv) {
+#define TCU_OVL(N)                                                                          \
+  case N:                                                                                  \
+    hipLaunchKernelGGL((overlap_probe_kernel<kMode, N>), dim3(blocks), dim3(512), 0, stream, \
+                       ops, iters, out);                                                   \
+    break;
+    TCU_OVL(0) TCU_OVL(1) TCU_OVL(2) TCU_OVL(3) TCU_OVL(4) TCU_OVL(6)
+#undef TCU_OVL
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 }  // namespace
 }  // namespace tcu
 
@@ -84,4 +160,27 @@ extern "C" __attribute__((visibility("default"))) int tcu_probe_mfma(int dtype, 
   else
     return -1;
   return hipGetLastError() == hipSuccess ? 0 : -6;
+}
+
+// ops: blocks * 512 * 3 16-byte words (device); out: blocks * 512 words
+// (device).  mode 0..3 as for overlap_probe_kernel; nv in {0, 1, 2, 3, 4, 6}
+// vector FMAs per matrix-core instruction.  Asynchronous on `stream`.
+// Returns 0, or -1 for bad arguments, -6 for a launch error.
+extern "C" __attribute__((visibility("default"))) int tcu_probe_overlap(int mode, int nv,
+                                                                        const void *ops, void *out,
+                                                                        int64_t iters, int blocks,
+                                                                        void *stream) {
+  if (!ops || !out || iters < 1 || blocks < 1 || mode < 0 || mode > 3) return -1;
+  const auto *o = static_cast<const tcu::u32x4 *>(ops);
+  auto *u = static_cast<unsigned *>(out);
+  hipStream_t st = (hipStream_t)stream;
+  hipError_t e;
+  switch (mode) {
+    case 0: e = tcu::launch_overlap<0>(nv, o, iters, u, blocks, st); break;
+    case 1: e = tcu::launch_overlap<1>(nv, o, iters, u, blocks, st); break;
+    case 2: e = tcu::launch_overlap<2>(nv, o, iters, u, blocks, st); break;
+    default: e = tcu::launch_overlap<3>(nv, o, iters, u, blocks, st); break;
+  }
+  if (e == hipErrorInvalidValue) return -1;
+  return e == hipSuccess ? 0 : -6;
 }
