@@ -595,7 +595,44 @@ def mfma_probe(iters: int = 100000, reps: int = 3) -> None:
             rate = flops / (ms * 1e-3) / 1e12
             res[f"{name}_{kind}"] = {"ms": ms, "T_per_s": rate, "frac_of_peak": rate / peak}
     res["overlap"] = overlap_probe(lib, blocks, st)
+    res["lds"] = lds_probe(lib, blocks, st)
     print(json.dumps(res), flush=True)
+
+
+def lds_probe(lib, blocks: int, st, iters: int = 20000, reps: int = 3) -> dict:
+    """LDS read rate per CU (libtcu_probe.so, tcu_probe_lds; one workgroup of
+    4, 8 or 16 waves per CU, 16 reads per wave and round): ds_read_b128 (1 KiB
+    per instruction) and ds_read_b64_tr_b16 (512 bytes), in bytes per ns per
+    CU and ns per instruction per CU."""
+    import ctypes
+    import torch
+    fn = lib.tcu_probe_lds
+    fn.restype = ctypes.c_int
+    fn.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_int,
+                   ctypes.c_void_p]
+    out = torch.empty(blocks * 1024, dtype=torch.int32, device="cuda")
+    res = {"iters": iters}
+    for kind, name, nbytes in ((0, "b128", 1024), (1, "tr16_b64", 512)):
+        for threads in (256, 512, 1024):
+            def run():
+                rc = fn(kind, out.data_ptr(), iters, blocks, threads, st.cuda_stream)
+                if rc != 0:
+                    raise RuntimeError(f"lds probe launch failed ({rc})")
+            run()
+            torch.cuda.synchronize()
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(st)
+            for _ in range(reps):
+                run()
+            e1.record(st)
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / reps
+            instr = (threads // 64) * iters * 16        # per CU
+            res[f"{name}_waves{threads // 64}"] = {
+                "ms": ms, "bytes_per_ns_per_cu": instr * nbytes / (ms * 1e6),
+                "ns_per_instruction_per_cu": ms * 1e6 / instr}
+    return res
 
 
 def overlap_probe(lib, blocks: int, st, iters: int = 10000, reps: int = 3) -> dict:

@@ -16,7 +16,8 @@
 //
 // A second probe (tcu_probe_overlap) measures whether binary32 vector ALU
 // work runs while the matrix core works: interleaved in one wave's
-// instruction stream, or issued by other waves on the same SIMD.
+// instruction stream, or issued by other waves on the same SIMD; a third
+// (tcu_probe_lds) the LDS read rate of the products' two fragment reads.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -122,6 +123,37 @@ overlap_probe_kernel(const u32x4 *__restrict__ ops, int64_t iters, unsigned *__r
   out[t] = h;
 }
 
+// LDS read-rate probe: every wave of a workgroup (4, 8 or 16 waves, one
+// workgroup per CU) reads 1 KiB per instruction with
+// ds_read_b128 (kKind 0; 64 lanes x 16 contiguous bytes, conflict-free) or
+// 512 bytes per instruction with ds_read_b64_tr_b16 (kKind 1; 64 lanes x 8
+// contiguous bytes), 16 instructions per round over a 64 KiB region, the
+// offset moving every round so that no read can be hoisted; the values are
+// folded into one word per lane.
+template <int kKind>
+__global__ __launch_bounds__(1024) void lds_probe_kernel(unsigned *__restrict__ out, int64_t iters) {
+  __shared__ __attribute__((aligned(16))) unsigned char s[65536];
+  for (int i = threadIdx.x; i < 65536 / 16; i += blockDim.x)
+    ((u32x4 *)s)[i] = u32x4{(unsigned)i, 1u, 2u, 3u};
+  __syncthreads();
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  u32x4 acc = {0u, 0u, 0u, 0u};
+  for (int64_t it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const int off = ((w * 16 + j + (int)(it & 63)) & 63) * 1024;   // < 64 KiB
+      if constexpr (kKind == 0) {
+        acc ^= *(const u32x4 *)(s + off + 16 * lane);
+      } else {
+        const u32x2 v = lds_read_tr16(s + off + 8 * lane);
+        acc[0] ^= v[0];
+        acc[1] ^= v[1];
+      }
+    }
+  }
+  out[(int64_t)blockIdx.x * blockDim.x + threadIdx.x] = acc[0] ^ acc[1] ^ acc[2] ^ acc[3];
+}
+
 template <int kMode>
 hipError_t launch_overlap(int nv, const u32x4 *ops, int64_t iters, unsigned *out, int blocks,
                           hipStream_t stream) {
@@ -183,4 +215,24 @@ extern "C" __attribute__((visibility("default"))) int tcu_probe_overlap(int mode
   }
   if (e == hipErrorInvalidValue) return -1;
   return e == hipSuccess ? 0 : -6;
+}
+
+// out: blocks * threads words (device).  kind 0: ds_read_b128, 1:
+// ds_read_b64_tr_b16; threads 256, 512 or 1024.  Every wave issues
+// 16 * iters LDS read instructions.  Asynchronous on `stream`.  Returns 0,
+// or -1 for bad arguments, -6 for a launch error.
+extern "C" __attribute__((visibility("default"))) int tcu_probe_lds(int kind, void *out,
+                                                                    int64_t iters, int blocks,
+                                                                    int threads, void *stream) {
+  if (!out || iters < 1 || blocks < 1 || (threads != 256 && threads != 512 && threads != 1024))
+    return -1;
+  auto *u = static_cast<unsigned *>(out);
+  hipStream_t st = (hipStream_t)stream;
+  if (kind == 0)
+    hipLaunchKernelGGL(tcu::lds_probe_kernel<0>, dim3(blocks), dim3(threads), 0, st, u, iters);
+  else if (kind == 1)
+    hipLaunchKernelGGL(tcu::lds_probe_kernel<1>, dim3(blocks), dim3(threads), 0, st, u, iters);
+  else
+    return -1;
+  return hipGetLastError() == hipSuccess ? 0 : -6;
 }
