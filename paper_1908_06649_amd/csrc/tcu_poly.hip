@@ -106,9 +106,9 @@ __global__ __launch_bounds__(kPolyThreads) void poly_kernel(const unsigned char 
   for (int64_t t0 = wave * U; t0 < nchunks; t0 += nwaves * U) {
     Run xh[U], xl[U];
     float yv[U], y16v[U], yg[U], acc[U], ystep[U];
-    // All U points first (clamped index, then a select), so the loads are
-    // in flight together.
-    // Points past np read as zero bits (+0 in both formats).
+    // All U points first, so their loads are in flight together; points
+    // past np read as zero bits (+0 in both formats), and a pass whose
+    // points all exist takes no range test.
     const int64_t p0 = t0 * 16;
     const bool whole = p0 + 16 * U <= np;   // every point of the pass exists
     const unsigned short *pp = pt16 + p0;
