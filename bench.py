@@ -23,7 +23,8 @@ JSON line:
              points with 4096 coefficients: TFLOP/s of the method's 2pn
              multiply-adds vs the bf16 matrix-core peak
   dft        DFT (tcu_dft, Theorem 7) of 16 complex64 vectors of 2^20: GB/s of
-             the levels' traffic (each of the ceil(log_32 n) levels reads and
+             the launches' traffic (each launch -- one of the ceil(log_32 n)
+             levels, or two consecutive levels fused through LDS -- reads and
              writes the array once) vs HBM peak, and 5 n log2 n GFLOP/s
   tc         transitive closure (tcu_transitive_closure, Theorem 5) of a
              random 8192-vertex digraph: GB/s of the D updates' algorithmic
@@ -119,6 +120,22 @@ def dft_levels(n: int, s: int) -> int:
     return levels
 
 
+def dft_launches(n: int, s: int) -> int:
+    """Launches of tcu_dft for length n with the library's default choice:
+    two consecutive full-radix levels in one launch where it pairs them (level
+    t+1 of full radix, and P_t >= 16 or P_t = 1 with at least 16 groups per
+    vector), else one launch per level.  Each launch reads and writes the
+    array once."""
+    levels, P, t, launches = dft_levels(n, s), 1, 1, 0
+    while t <= levels:
+        n2 = n // P // s
+        pair = t < levels and n2 >= s and (P >= 16 or (P == 1 and n2 // s >= 16))
+        P *= s * s if pair else (s if t < levels else n // P)
+        t += 2 if pair else 1
+        launches += 1
+    return launches
+
+
 def algorithmic(spec: dict):
     """(work per call in flop/op, bytes per call) that the method must do."""
     ib = 1 if spec.get("dtype", "i8") == "i8" else 2
@@ -128,7 +145,7 @@ def algorithmic(spec: dict):
         return 2.0 * n * s * s, n * s * ib + s * s * ib + n * s * ob
     if spec["kind"] == "dft":
         n, b = spec["n"], spec["batch"]
-        return 5.0 * b * n * math.log2(n), dft_levels(n, spec["s"]) * 2 * 8 * b * n
+        return 5.0 * b * n * math.log2(n), dft_launches(n, spec["s"]) * 2 * 8 * b * n
     if spec["kind"] == "tc":
         # per pivot band of up to 256 vertices: the D update reads and writes
         # every off-band entry once, the panel updates their band entries
@@ -297,8 +314,9 @@ def measure(name: str, steps: int, warmup: int) -> dict:
                                  "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS,
                                  "traffic": counted_traffic(name, kind)},
                     "gflops_5nlogn": flops / (ms * 1e-3) / 1e9,
-                    "launches_per_call": dft_levels(sp["n"], sp["s"]),
-                    "algorithmic_bytes_per_launch": nbytes / dft_levels(sp["n"], sp["s"])})
+                    "levels": dft_levels(sp["n"], sp["s"]),
+                    "launches_per_call": dft_launches(sp["n"], sp["s"]),
+                    "algorithmic_bytes_per_launch": nbytes / dft_launches(sp["n"], sp["s"])})
     elif kind == "tc":
         gbs = nbytes / (ms * 1e-3) / 1e9
         out.update({"value": gbs, "unit": "GB/s",

@@ -373,6 +373,9 @@ const char *tcu_strerror(int status);
  *     (0: by size; 1: none).
  *   TCU_KNOB_CHECK_POINTERS: 1 = check every operand with
  *     tcu_check_device_range before launching, 0 = no checks.
+ *   TCU_KNOB_DFT_PAIRS: 1 = every DFT level its own launch; 0 = two
+ *     consecutive full-radix levels in one launch where possible (the same
+ *     result, bit for bit).
  * Returns TCU_OK, or TCU_ERR_UNSUPPORTED for an unknown knob or a value
  * out of range (the knob is then unchanged); tcu_get_knob returns -1 for an
  * unknown knob.  Changing a knob while another thread issues calls is safe
@@ -382,7 +385,8 @@ enum {
     TCU_KNOB_PP_GRID = 1,
     TCU_KNOB_SPLIT_K = 2,
     TCU_KNOB_TAIL_SPLIT = 3,
-    TCU_KNOB_CHECK_POINTERS = 4
+    TCU_KNOB_CHECK_POINTERS = 4,
+    TCU_KNOB_DFT_PAIRS = 5
 };
 enum { TCU_PATH_AUTO = 0, TCU_PATH_FULL_TILE = 1, TCU_PATH_GENERAL = 2, TCU_PATH_RING = 3 };
 int tcu_check_device_range(const void *p, int64_t bytes);

@@ -31,13 +31,13 @@ thread_local UnitConfig g_cfg;
 // Test overrides and the pointer-check switch (tcu_set_knob).  Pointer
 // checks start on when TCU_DEBUG holds a nonzero integer at load time; the
 // environment is read only here, once.
-constexpr int kKnobs = 5;
+constexpr int kKnobs = 6;
 int initial_knob(int k) {
   if (k != TCU_KNOB_CHECK_POINTERS) return 0;
   const char *v = std::getenv("TCU_DEBUG");
   return v && std::atoi(v) != 0 ? 1 : 0;
 }
-std::atomic<int> g_knob[kKnobs] = {{0}, {0}, {0}, {0}, {initial_knob(TCU_KNOB_CHECK_POINTERS)}};
+std::atomic<int> g_knob[kKnobs] = {{0}, {0}, {0}, {0}, {initial_knob(TCU_KNOB_CHECK_POINTERS)}, {0}};
 
 std::atomic<int64_t> g_calls{0};
 std::atomic<int64_t> g_square_calls{0};
@@ -522,7 +522,8 @@ TCU_EXPORT int tcu_check_device_range(const void *p, int64_t bytes) {
 TCU_EXPORT int tcu_set_knob(int knob, int value) {
   if (knob < 0 || knob >= kKnobs || value < 0) return TCU_ERR_UNSUPPORTED;
   if (knob == TCU_KNOB_GEMM_KERNEL && value > TCU_PATH_RING) return TCU_ERR_UNSUPPORTED;
-  if (knob == TCU_KNOB_CHECK_POINTERS && value > 1) return TCU_ERR_UNSUPPORTED;
+  if ((knob == TCU_KNOB_CHECK_POINTERS || knob == TCU_KNOB_DFT_PAIRS) && value > 1)
+    return TCU_ERR_UNSUPPORTED;
   g_knob[knob].store(value, std::memory_order_relaxed);
   return TCU_OK;
 }

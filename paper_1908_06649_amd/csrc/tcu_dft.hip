@@ -5,8 +5,9 @@
 // The section arranges x as an s x (n/s) matrix, replaces every column by
 // its DFT -- the tall product X^T W_s, n/s rows through the unit -- scales
 // entry (r, c) by the twiddle w_n^(r c), transposes, and recurses on the s
-// rows (a last level of radix n/s^(L-1) <= s).  Here each level is one
-// launch that reads the whole array and writes it reordered (a Stockham
+// rows (a last level of radix n/s^(L-1) <= s).  Here each level -- or two
+// consecutive full-radix levels at once (dft_pair_kernel, through LDS) -- is
+// one launch that reads the whole array and writes it reordered (a Stockham
 // ordering: the digits of k already produced are kept as the fastest-varying
 // index), so the last level leaves y in natural order with no separate
 // transpose.  With n = R_1 ... R_L, P_t = R_1 ... R_(t-1) and N_t = n / P_t:
@@ -50,35 +51,29 @@ __device__ __forceinline__ f32x2 cmul(f32x2 a, f32x2 b) {
   return f32x2{a[0] * b[0] - a[1] * b[1], a[0] * b[1] + a[1] * b[0]};
 }
 
-// One level.  n, R, P, N_t are powers of two and enter as their base-2
-// logarithms; ntrans = batch * n / R transforms, 16 per wave step.
+// Shapes of a radix-S step on the unit: a lane holds kRun consecutive
+// contracted elements, and the S output frequencies come in kH halves of 16.
 template <int S>
-__global__ __launch_bounds__(kDftThreads) void dft_level_kernel(
-    const f32x2 *__restrict__ src, f32x2 *__restrict__ dst, int lg_n, int lg_r, int lg_p,
-    int64_t ntrans) {
-  constexpr int kRun = S == 32 ? 8 : 4;   // contracted elements per lane
-  constexpr int kH = S / 16;              // 16-frequency halves
-  constexpr int kWords = kRun / 2;
+struct DftShape {
+  static constexpr int kRun = S == 32 ? 8 : 4;   // contracted elements per lane
+  static constexpr int kH = S / 16;              // 16-frequency halves
+  static constexpr int kWords = kRun / 2;
   typedef typename std::conditional<kRun == 8, u32x4, u32x2>::type Run;
-  __shared__ f32x2 wtab[S];               // w_R^m, m < R
+};
 
-  const int R = 1 << lg_r;
-  const int lg_pv = lg_n - lg_r;          // log2 of the transforms per vector
-  const int lg_nt = lg_n - lg_p;          // log2 N_t
-  const int64_t nt_mask = ((int64_t)1 << lg_nt) - 1;
-  const bool last = lg_nt == lg_r;        // N_t = R: no twiddles
-  const bool contiguous = lg_p == 0 && R >= 4;   // a lane's 4 outputs are adjacent
-
-  if (threadIdx.x < (unsigned)R) wtab[threadIdx.x] = twiddle(threadIdx.x, R);
-  __syncthreads();
-
-  const int lane = threadIdx.x & 63;
-  const int r = lane & 15, g = lane >> 4;
-  const SplitConsts sc = split_consts();
-
-  // Weights operand: row k = 16h + r, contracted run j = kRun g + e, value
-  // w_R^(j k) (zero outside R x R), as hi/lo words; -Wi for the real part.
-  Run wr_h[kH], wr_l[kH], wi_h[kH], wi_l[kH], ni_h[kH], ni_l[kH];
+// The weights operand W_R (R <= S) as hi/lo words: row k = 16h + r of the
+// unit operand, contracted run j = kRun g + e, value w_R^(j k) (zero
+// outside R x R); -Wi for the real part.  wtab[m] = w_R^m.
+template <int S>
+struct DftWeights {
+  typedef typename DftShape<S>::Run Run;
+  Run wr_h[DftShape<S>::kH], wr_l[DftShape<S>::kH], wi_h[DftShape<S>::kH],
+      wi_l[DftShape<S>::kH], ni_h[DftShape<S>::kH], ni_l[DftShape<S>::kH];
+};
+template <int S>
+__device__ __forceinline__ void dft_weights(DftWeights<S> &W, const f32x2 *wtab, int R, int r,
+                                            int g, SplitConsts sc) {
+  constexpr int kRun = DftShape<S>::kRun, kH = DftShape<S>::kH, kWords = DftShape<S>::kWords;
 #pragma unroll
   for (int h = 0; h < kH; ++h) {
     float cr[kRun], ci[kRun];
@@ -94,15 +89,100 @@ __global__ __launch_bounds__(kDftThreads) void dft_level_kernel(
     for (int q = 0; q < kWords; ++q) {
       unsigned hi, lo;
       split_bf16x2(cr[2 * q], cr[2 * q + 1], hi, lo, sc);
-      wr_h[h][q] = hi;
-      wr_l[h][q] = lo;
+      W.wr_h[h][q] = hi;
+      W.wr_l[h][q] = lo;
       split_bf16x2(ci[2 * q], ci[2 * q + 1], hi, lo, sc);
-      wi_h[h][q] = hi;
-      wi_l[h][q] = lo;
-      ni_h[h][q] = hi ^ 0x80008000u;   // -Wi: flip both signs
-      ni_l[h][q] = lo ^ 0x80008000u;
+      W.wi_h[h][q] = hi;
+      W.wi_l[h][q] = lo;
+      W.ni_h[h][q] = hi ^ 0x80008000u;   // -Wi: flip both signs
+      W.ni_l[h][q] = lo ^ 0x80008000u;
     }
   }
+}
+
+// One transform column of the unit (lane (r, g) holds its elements
+// j = kRun g + e): the data as hi/lo words, then for half h the real and
+// imaginary parts of outputs 16h + 4g + i, i < 4 (the matrix-core output
+// layout), each real product formed as hi*hi + hi*lo + lo*hi.
+template <int S>
+struct DftData {
+  typename DftShape<S>::Run xr_h, xr_l, xi_h, xi_l;
+};
+template <int S>
+__device__ __forceinline__ void dft_data(DftData<S> &X, const float *xr, const float *xi,
+                                         SplitConsts sc) {
+#pragma unroll
+  for (int q = 0; q < DftShape<S>::kWords; ++q) {
+    unsigned hi, lo;
+    split_bf16x2(xr[2 * q], xr[2 * q + 1], hi, lo, sc);
+    X.xr_h[q] = hi;
+    X.xr_l[q] = lo;
+    split_bf16x2(xi[2 * q], xi[2 * q + 1], hi, lo, sc);
+    X.xi_h[q] = hi;
+    X.xi_l[q] = lo;
+  }
+}
+template <int S>
+__device__ __forceinline__ void dft_half(const DftWeights<S> &W, const DftData<S> &X, int h,
+                                         f32x4 &re, f32x4 &im) {
+  typedef typename DftShape<S>::Run Run;
+  auto mma = [&](const Run &w, const Run &x, f32x4 d) __attribute__((always_inline)) {
+    if constexpr (S == 32)
+      return mfma_k32(TCU_BF16_F32, w, x, d);
+    else
+      return mfma_k16(TCU_BF16_F32, w, x, d);
+  };
+  re = f32x4{0.f, 0.f, 0.f, 0.f};
+  im = f32x4{0.f, 0.f, 0.f, 0.f};
+  re = mma(W.wr_h[h], X.xr_h, re);
+  re = mma(W.wr_h[h], X.xr_l, re);
+  re = mma(W.wr_l[h], X.xr_h, re);
+  re = mma(W.ni_h[h], X.xi_h, re);
+  re = mma(W.ni_h[h], X.xi_l, re);
+  re = mma(W.ni_l[h], X.xi_h, re);
+  im = mma(W.wi_h[h], X.xr_h, im);
+  im = mma(W.wi_h[h], X.xr_l, im);
+  im = mma(W.wi_l[h], X.xr_h, im);
+  im = mma(W.wr_h[h], X.xi_h, im);
+  im = mma(W.wr_h[h], X.xi_l, im);
+  im = mma(W.wr_l[h], X.xi_h, im);
+}
+// Outputs k0 .. k0+3 of transform J times the twiddles w_(N_t)^(J k):
+// w^(J k0), then repeated products with step = w^J.
+__device__ __forceinline__ void dft_twiddle4(f32x2 (&y)[4], int64_t J, int k0, int lg_nt,
+                                             int64_t nt_mask, f32x2 step) {
+  f32x2 w = twiddle((J * k0) & nt_mask, (int64_t)1 << lg_nt);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    y[i] = cmul(y[i], w);
+    if (i < 3) w = cmul(w, step);
+  }
+}
+
+// One level.  n, R, P, N_t are powers of two and enter as their base-2
+// logarithms; ntrans = batch * n / R transforms, 16 per wave step.
+template <int S>
+__global__ __launch_bounds__(kDftThreads) void dft_level_kernel(
+    const f32x2 *__restrict__ src, f32x2 *__restrict__ dst, int lg_n, int lg_r, int lg_p,
+    int64_t ntrans) {
+  constexpr int kRun = DftShape<S>::kRun, kH = DftShape<S>::kH;
+  __shared__ f32x2 wtab[S];               // w_R^m, m < R
+
+  const int R = 1 << lg_r;
+  const int lg_pv = lg_n - lg_r;          // log2 of the transforms per vector
+  const int lg_nt = lg_n - lg_p;          // log2 N_t
+  const int64_t nt_mask = ((int64_t)1 << lg_nt) - 1;
+  const bool last = lg_nt == lg_r;        // N_t = R: no twiddles
+  const bool contiguous = lg_p == 0 && R >= 4;   // a lane's 4 outputs are adjacent
+
+  if (threadIdx.x < (unsigned)R) wtab[threadIdx.x] = twiddle(threadIdx.x, R);
+  __syncthreads();
+
+  const int lane = threadIdx.x & 63;
+  const int r = lane & 15, g = lane >> 4;
+  const SplitConsts sc = split_consts();
+  DftWeights<S> W;
+  dft_weights<S>(W, wtab, R, r, g, sc);
 
   const int64_t wave = (int64_t)blockIdx.x * (kDftThreads / 64) + (threadIdx.x >> 6);
   const int64_t nwaves = (int64_t)gridDim.x * (kDftThreads / 64);
@@ -113,7 +193,7 @@ __global__ __launch_bounds__(kDftThreads) void dft_level_kernel(
     const int64_t b = live ? tr >> lg_pv : 0;
     const int64_t c = live ? tr & (((int64_t)1 << lg_pv) - 1) : 0;
     const f32x2 *vin = src + (b << lg_n) + c;
-    // data: a[j], j = kRun g + e, as hi/lo words of the real and imaginary parts
+    // data: a[j], j = kRun g + e
     float xr[kRun], xi[kRun];
 #pragma unroll
     for (int e = 0; e < kRun; ++e) {
@@ -123,55 +203,21 @@ __global__ __launch_bounds__(kDftThreads) void dft_level_kernel(
       xr[e] = v[0];
       xi[e] = v[1];
     }
-    Run xr_h, xr_l, xi_h, xi_l;
-#pragma unroll
-    for (int q = 0; q < kWords; ++q) {
-      unsigned hi, lo;
-      split_bf16x2(xr[2 * q], xr[2 * q + 1], hi, lo, sc);
-      xr_h[q] = hi;
-      xr_l[q] = lo;
-      split_bf16x2(xi[2 * q], xi[2 * q + 1], hi, lo, sc);
-      xi_h[q] = hi;
-      xi_l[q] = lo;
-    }
+    DftData<S> X;
+    dft_data<S>(X, xr, xi, sc);
     const int64_t J = c >> lg_p, K = c & (((int64_t)1 << lg_p) - 1);
     f32x2 *vout = dst + (b << lg_n) + ((J << lg_r) << lg_p) + K;
-    // twiddle w_(N_t)^(J k) for k = k0 + i: w^(J k0) times step^i, step = w^J
     const f32x2 step = last ? f32x2{1.f, 0.f} : twiddle(J & nt_mask, (int64_t)1 << lg_nt);
 #pragma unroll
     for (int h = 0; h < kH; ++h) {
-      f32x4 re = {0.f, 0.f, 0.f, 0.f}, im = {0.f, 0.f, 0.f, 0.f};
-      auto mma = [&](const Run &w, const Run &x, f32x4 d) __attribute__((always_inline)) {
-        if constexpr (S == 32)
-          return mfma_k32(TCU_BF16_F32, w, x, d);
-        else
-          return mfma_k16(TCU_BF16_F32, w, x, d);
-      };
-      re = mma(wr_h[h], xr_h, re);
-      re = mma(wr_h[h], xr_l, re);
-      re = mma(wr_l[h], xr_h, re);
-      re = mma(ni_h[h], xi_h, re);
-      re = mma(ni_h[h], xi_l, re);
-      re = mma(ni_l[h], xi_h, re);
-      im = mma(wi_h[h], xr_h, im);
-      im = mma(wi_h[h], xr_l, im);
-      im = mma(wi_l[h], xr_h, im);
-      im = mma(wr_h[h], xi_h, im);
-      im = mma(wr_h[h], xi_l, im);
-      im = mma(wr_l[h], xi_h, im);
+      f32x4 re, im;
+      dft_half<S>(W, X, h, re, im);
       const int k0 = 16 * h + 4 * g;
       if (!live || k0 >= R) continue;
       f32x2 y[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) y[i] = f32x2{re[i], im[i]};
-      if (!last) {
-        f32x2 w = twiddle((J * k0) & nt_mask, (int64_t)1 << lg_nt);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          y[i] = cmul(y[i], w);
-          if (i < 3) w = cmul(w, step);
-        }
-      }
+      if (!last) dft_twiddle4(y, J, k0, lg_nt, nt_mask, step);
       if (contiguous) {   // outputs k0 .. k0+3 of transform J: 32 adjacent bytes
         f32x4 *o = (f32x4 *)(vout + k0);
         o[0] = f32x4{y[0][0], y[0][1], y[1][0], y[1][1]};
@@ -185,6 +231,156 @@ __global__ __launch_bounds__(kDftThreads) void dft_level_kernel(
   }
 }
 
+
+// Two consecutive levels t, t+1 of radix S in one launch (both R = S, and
+// P_t >= 16 or P_t = 1).  With P = P_t, N' = N_t / S and P' = P S, level
+// t+1's transform (J', K' = k P + K) reads output k of level t's
+// transforms J = J' + j' (N'/S), j' < S, with the same K.  So the S x S
+// values of group (J', K) -- level t's transforms J (rows j') by their
+// outputs k -- are formed and consumed inside one workgroup, through LDS:
+//   * a workgroup takes 16 groups at once: 16 consecutive K (P >= 16,
+//     kLaneK) or 16 consecutive J' (P = 1), so that the level-t loads and
+//     the level-(t+1) stores of the 16 matrix-core columns are contiguous;
+//   * level t: S steps j' (a wave takes every 4th), each the 16 groups'
+//     transforms J = J' + j' (N'/S) as in dft_level_kernel (all of a wave's
+//     loads issued first), outputs times w_(N_t)^(J k) into the LDS tile
+//     T[group][j'][k];
+//   * level t+1: S steps, each 16 transforms over j' read from the tiles
+//     (kLaneK: output k of the 16 groups; otherwise 16 consecutive k of one
+//     group), outputs times w_(N')^(J' k') unless it is the last level,
+//     stored in level t+1's Stockham order.
+// Every value takes the same operations as with two dft_level_kernel
+// launches (the same weights, products, twiddles, binary32 between the
+// levels), so the result is the same bit for bit; only the array's trip
+// through HBM between the two levels is saved.
+constexpr int kPairGroups = 16;
+template <int S>
+constexpr int pair_row() { return S + 1; }                          // j' rows, padded
+template <int S>
+constexpr int pair_group() { return S * pair_row<S>() + 1; }       // one group's tile
+
+constexpr int kPairThreads = 512;   // 8 waves: two per SIMD
+
+template <int S, bool kLaneK>
+__global__ __launch_bounds__(kPairThreads) void dft_pair_kernel(
+    const f32x2 *__restrict__ src, f32x2 *__restrict__ dst, int lg_n, int lg_p, int64_t ntiles,
+    int last2) {
+  constexpr int kRun = DftShape<S>::kRun, kH = DftShape<S>::kH;
+  constexpr int lg_s = S == 32 ? 5 : 4;
+  constexpr int kWaves = kPairThreads / 64;
+  constexpr int kSteps = S / kWaves;                // level steps per wave
+  constexpr int kRow = pair_row<S>(), kGrp = pair_group<S>();
+  __shared__ f32x2 wtab[S];
+  __shared__ f32x2 tile[kPairGroups * kGrp];
+
+  const int lg_nt = lg_n - lg_p;             // level t: N_t
+  const int lg_n2 = lg_nt - lg_s;            // level t+1: N' = N_t / S
+  const int64_t nt_mask = ((int64_t)1 << lg_nt) - 1;
+  const int64_t n2_mask = ((int64_t)1 << lg_n2) - 1;
+  const int lg_jp = lg_n2 - lg_s;            // log2 (N'/S): the J' range
+  const int lg_pv = lg_n - lg_s;             // n / S: level t's element stride
+
+  if (threadIdx.x < (unsigned)S) wtab[threadIdx.x] = twiddle(threadIdx.x, S);
+  __syncthreads();
+  const int lane = threadIdx.x & 63;
+  const int r = lane & 15, g = lane >> 4;
+  const int wv = threadIdx.x >> 6;
+  const SplitConsts sc = split_consts();
+  DftWeights<S> W;
+  dft_weights<S>(W, wtab, S, r, g, sc);
+
+  // tiles per vector: (N'/S) (P/16) with kLaneK, (N'/S)/16 otherwise
+  const int lg_tpv = kLaneK ? lg_jp + lg_p - 4 : lg_jp - 4;
+  for (int64_t q = blockIdx.x; q < ntiles; q += gridDim.x) {
+    const int64_t b = q >> lg_tpv;
+    const int64_t ql = q & (((int64_t)1 << lg_tpv) - 1);
+    const f32x2 *vsrc = src + (b << lg_n);
+    f32x2 *vdst = dst + (b << lg_n);
+    // this lane's group: J'_r and K_r
+    const int64_t Jp = kLaneK ? ql >> (lg_p - 4) : (ql << 4) + r;
+    const int64_t Kr = kLaneK ? ((ql & (((int64_t)1 << (lg_p - 4)) - 1)) << 4) + r : 0;
+
+    // ---- level t: the wave's steps j' = wv + kWaves i, loads issued first
+    f32x2 v[kSteps][kRun];
+#pragma unroll
+    for (int i = 0; i < kSteps; ++i) {
+      const int64_t J = Jp + ((int64_t)(wv + kWaves * i) << lg_jp);
+      const f32x2 *vin = vsrc + (J << lg_p) + Kr;
+#pragma unroll
+      for (int e = 0; e < kRun; ++e) v[i][e] = vin[(int64_t)(kRun * g + e) << lg_pv];
+    }
+#pragma unroll
+    for (int i = 0; i < kSteps; ++i) {
+      const int jp = wv + kWaves * i;
+      const int64_t J = Jp + ((int64_t)jp << lg_jp);
+      float xr[kRun], xi[kRun];
+#pragma unroll
+      for (int e = 0; e < kRun; ++e) {
+        xr[e] = v[i][e][0];
+        xi[e] = v[i][e][1];
+      }
+      DftData<S> X;
+      dft_data<S>(X, xr, xi, sc);
+      const f32x2 step = twiddle(J & nt_mask, (int64_t)1 << lg_nt);
+#pragma unroll
+      for (int h = 0; h < kH; ++h) {
+        f32x4 re, im;
+        dft_half<S>(W, X, h, re, im);
+        const int k0 = 16 * h + 4 * g;
+        f32x2 y[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) y[e] = f32x2{re[e], im[e]};
+        dft_twiddle4(y, J, k0, lg_nt, nt_mask, step);
+        f32x2 *t = tile + r * kGrp + jp * kRow + k0;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) t[e] = y[e];
+      }
+    }
+    __syncthreads();
+
+    // ---- level t+1: the wave's steps
+#pragma unroll
+    for (int i = 0; i < kSteps; ++i) {
+      const int ch = wv + kWaves * i;
+      int grp, k;
+      if constexpr (kLaneK) {
+        grp = r;
+        k = ch;
+      } else {
+        grp = ch / (S / 16);
+        k = 16 * (ch % (S / 16)) + r;
+      }
+      const int64_t J2 = kLaneK ? Jp : (ql << 4) + grp;          // level t+1's J'
+      const int64_t K2 = ((int64_t)k << lg_p) + (kLaneK ? Kr : 0);
+      float xr[kRun], xi[kRun];
+      const f32x2 *t = tile + grp * kGrp + k;
+#pragma unroll
+      for (int e = 0; e < kRun; ++e) {
+        const f32x2 a = t[(kRun * g + e) * kRow];
+        xr[e] = a[0];
+        xi[e] = a[1];
+      }
+      DftData<S> X;
+      dft_data<S>(X, xr, xi, sc);
+      f32x2 *vout = vdst + ((J2 << lg_s) << (lg_p + lg_s)) + K2;
+      const f32x2 step = last2 ? f32x2{1.f, 0.f} : twiddle(J2 & n2_mask, (int64_t)1 << lg_n2);
+#pragma unroll
+      for (int h = 0; h < kH; ++h) {
+        f32x4 re, im;
+        dft_half<S>(W, X, h, re, im);
+        const int k0 = 16 * h + 4 * g;
+        f32x2 y[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) y[e] = f32x2{re[e], im[e]};
+        if (!last2) dft_twiddle4(y, J2, k0, lg_n2, n2_mask, step);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) vout[(int64_t)(k0 + e) << (lg_p + lg_s)] = y[e];
+      }
+    }
+    __syncthreads();   // the tiles are rewritten by the next iteration
+  }
+}
+
 // Scratch of the allocation-free DFT (tcu_dft_noalloc): the levels' second
 // buffer.  In host code this name is only a stand-in for the symbol; the
 // array's device address comes from hipGetSymbolAddress, once per device.
@@ -194,6 +390,31 @@ int ilog2(int64_t v) {
   int l = 0;
   while (((int64_t)1 << l) < v) ++l;
   return l;
+}
+
+// Whether levels t, t+1 (radix S each, P = P_t) run as one pair launch:
+// both full radix, and a coalesced lane order exists (16 consecutive K, or
+// P = 1 with at least 16 groups J' per vector).
+bool pair_ok(int64_t n, int s, int64_t P) {
+  const int64_t n2 = n / P / s;   // N' = N_t / s
+  if (n2 < s) return false;       // level t+1 would not have full radix
+  if (knob(TCU_KNOB_DFT_PAIRS) == 1) return false;   // test override: single levels
+  return P >= 16 || (P == 1 && n2 / s >= 16);
+}
+
+template <int S>
+hipError_t launch_pair(const f32x2 *src, f32x2 *dst, int64_t n, int64_t P, int64_t batch,
+                       bool last2, hipStream_t stream, int num_cus) {
+  const int64_t ntiles = batch * (n / ((int64_t)S * S)) / kPairGroups;
+  const int64_t cap = num_cus;      // one workgroup per CU (the tiles take most of the LDS)
+  const int blocks = (int)(ntiles < cap ? ntiles : cap);
+  if (P >= 16)
+    hipLaunchKernelGGL((dft_pair_kernel<S, true>), dim3(blocks), dim3(kPairThreads), 0, stream,
+                       src, dst, ilog2(n), ilog2(P), ntiles, last2 ? 1 : 0);
+  else
+    hipLaunchKernelGGL((dft_pair_kernel<S, false>), dim3(blocks), dim3(kPairThreads), 0, stream,
+                       src, dst, ilog2(n), ilog2(P), ntiles, last2 ? 1 : 0);
+  return hipGetLastError();
 }
 
 template <int S>
@@ -244,17 +465,43 @@ hipError_t launch_dft(const void *x, void *y, void *work, int64_t n, int64_t bat
                       hipStream_t stream, int num_cus) {
   if (n <= 0 || batch <= 0) return hipSuccess;
   const int L = dft_levels(n, s);
+  // Launches: levels taken two at a time where pair_ok holds, else one
+  // (decided once, before anything is launched).
+  bool pairs[64];
+  int launches = 0;
+  {
+    int64_t P = 1;
+    for (int t = 1; t <= L;) {
+      const bool pair = t < L && pair_ok(n, s, P);
+      P *= pair ? (int64_t)s * s : (t < L ? s : n / P);
+      t += pair ? 2 : 1;
+      pairs[launches++] = pair;
+    }
+  }
   int64_t P = 1;
   const f32x2 *src = (const f32x2 *)x;
-  for (int t = 1; t <= L; ++t) {
-    const int R = (int)(t < L ? s : n / P);
-    // the levels alternate between work and y so that the last lands in y
-    f32x2 *dst = (f32x2 *)(((L - t) % 2 == 0) ? y : work);
-    const hipError_t e = s == 32 ? launch_level<32>(src, dst, n, R, P, batch, stream, num_cus)
-                                 : launch_level<16>(src, dst, n, R, P, batch, stream, num_cus);
+  int launch = 0;
+  for (int t = 1; t <= L;) {
+    const bool pair = pairs[launch];
+    // the launches alternate between work and y so that the last lands in y
+    ++launch;
+    f32x2 *dst = (f32x2 *)(((launches - launch) % 2 == 0) ? y : work);
+    hipError_t e;
+    if (pair) {
+      const bool last2 = t + 1 == L;
+      e = s == 32 ? launch_pair<32>(src, dst, n, P, batch, last2, stream, num_cus)
+                  : launch_pair<16>(src, dst, n, P, batch, last2, stream, num_cus);
+      P *= (int64_t)s * s;
+      t += 2;
+    } else {
+      const int R = (int)(t < L ? s : n / P);
+      e = s == 32 ? launch_level<32>(src, dst, n, R, P, batch, stream, num_cus)
+                  : launch_level<16>(src, dst, n, R, P, batch, stream, num_cus);
+      P *= R;
+      t += 1;
+    }
     if (e != hipSuccess) return e;
     src = dst;
-    P *= R;
   }
   return hipSuccess;
 }

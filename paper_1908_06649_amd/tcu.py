@@ -51,6 +51,7 @@ TCU_KNOB_PP_GRID = 1
 TCU_KNOB_SPLIT_K = 2
 TCU_KNOB_TAIL_SPLIT = 3
 TCU_KNOB_CHECK_POINTERS = 4
+TCU_KNOB_DFT_PAIRS = 5
 TCU_PATH_AUTO = 0
 TCU_PATH_FULL_TILE = 1
 TCU_PATH_GENERAL = 2

@@ -80,7 +80,7 @@ def test_knobs_set_get_and_reject(L):
     range are rejected and leave the knob unchanged."""
     for knob, good in ((tcu.TCU_KNOB_GEMM_KERNEL, tcu.TCU_PATH_RING), (tcu.TCU_KNOB_PP_GRID, 3),
                        (tcu.TCU_KNOB_SPLIT_K, 4), (tcu.TCU_KNOB_TAIL_SPLIT, 1),
-                       (tcu.TCU_KNOB_CHECK_POINTERS, 1)):
+                       (tcu.TCU_KNOB_CHECK_POINTERS, 1), (tcu.TCU_KNOB_DFT_PAIRS, 1)):
         start = L.tcu_get_knob(knob)
         assert L.tcu_set_knob(knob, good) == tcu.TCU_OK and L.tcu_get_knob(knob) == good
         assert L.tcu_set_knob(knob, -1) == tcu.TCU_ERR_UNSUPPORTED
@@ -88,9 +88,10 @@ def test_knobs_set_get_and_reject(L):
         assert L.tcu_set_knob(knob, start) == tcu.TCU_OK
     assert L.tcu_set_knob(tcu.TCU_KNOB_GEMM_KERNEL, 4) == tcu.TCU_ERR_UNSUPPORTED
     assert L.tcu_set_knob(tcu.TCU_KNOB_CHECK_POINTERS, 2) == tcu.TCU_ERR_UNSUPPORTED
-    assert L.tcu_set_knob(5, 0) == tcu.TCU_ERR_UNSUPPORTED
+    assert L.tcu_set_knob(tcu.TCU_KNOB_DFT_PAIRS, 2) == tcu.TCU_ERR_UNSUPPORTED
+    assert L.tcu_set_knob(6, 0) == tcu.TCU_ERR_UNSUPPORTED
     assert L.tcu_set_knob(-1, 0) == tcu.TCU_ERR_UNSUPPORTED
-    assert L.tcu_get_knob(5) == -1 and L.tcu_get_knob(-1) == -1
+    assert L.tcu_get_knob(6) == -1 and L.tcu_get_knob(-1) == -1
 
 
 def test_debug_env_turns_pointer_checks_on():

@@ -44,9 +44,10 @@ def test_algorithmic_rect_poly_tc_dft():
     # the normalizing pass
     w, b = bench.algorithmic({"kind": "tc", "n": 256})
     assert w == 2 * 256 ** 3 and b == 2 * 256 * 256 + 2 * 256 * 256
-    # DFT: each of the 4 radix-32 levels of 2^20 reads and writes the array
+    # DFT: the 4 radix-32 levels of 2^20 run as 2 launches (levels 1-2 and
+    # 3-4 fused), each reading and writing the array once
     w, b = bench.algorithmic(inputs.DFT_WORKLOADS["dft_c64_n1048576_b16_s32"])
-    assert b == 4 * 2 * 8 * 16 * (1 << 20) and w == 5 * 16 * (1 << 20) * 20
+    assert b == 2 * 2 * 8 * 16 * (1 << 20) and w == 5 * 16 * (1 << 20) * 20
 
 
 @pytest.mark.parametrize("n,s,levels", [(1, 32, 1), (32, 32, 1), (64, 32, 2), (1024, 32, 2),
@@ -54,6 +55,15 @@ def test_algorithmic_rect_poly_tc_dft():
                                         (16, 16, 1), (1 << 30, 32, 6)])
 def test_dft_levels(n, s, levels):
     assert bench.dft_levels(n, s) == levels
+
+
+@pytest.mark.parametrize("n,s,launches", [(32, 32, 1), (1024, 32, 2), (1 << 14, 32, 2),
+                                          (1 << 15, 32, 2), (1 << 20, 32, 2), (1 << 12, 16, 2),
+                                          (1 << 16, 16, 2), (1 << 20, 16, 3), (2048, 16, 3)])
+def test_dft_launches(n, s, launches):
+    """Pairs of full-radix levels share a launch where the library fuses them
+    (the pair conditions of the DFT launcher)."""
+    assert bench.dft_launches(n, s) == launches
 
 
 def test_multi_gpu_request_exits_with_a_message():

@@ -96,3 +96,25 @@ def test_dft_workload(name):
     rep = compare.check_dft(x.numpy(), got)
     assert rep["freqs_checked"] >= 64
     print(name, rep)
+
+
+# Sizes where two consecutive full-radix levels run as one launch: for s = 32
+# the first two levels from n = 2^14 (16 groups J' per vector) and levels 3-4
+# at n = 2^20 (P = 2^10); for s = 16 from n = 2^12, and levels 2-3 at
+# n = 2^16 (P = 16).
+PAIR_CASES = [(1 << 12, 3, 16), (1 << 14, 2, 16), (1 << 16, 2, 16), (1 << 14, 3, 32),
+              (1 << 15, 2, 32), (1 << 20, 2, 32), (1 << 18, 1, 16)]
+
+
+@pytest.mark.parametrize("n,batch,s", PAIR_CASES)
+def test_dft_level_pairs_bit_identical(knobs, n, batch, s):
+    """Two levels in one launch (the default where possible) give the same
+    bits as one launch per level (TCU_KNOB_DFT_PAIRS = 1): every value takes
+    the same operations either way."""
+    x = inputs.complex_signal(batch, n, seed=n + 7 * batch + s)
+    paired = run_dft(x, s)
+    knobs(tcu.TCU_KNOB_DFT_PAIRS, 1)
+    single = run_dft(x, s)
+    assert np.array_equal(paired.view(np.uint64), single.view(np.uint64))
+    rep = compare.check_dft(x.numpy(), paired)
+    assert rep["max_rel_frob"] <= 1e-4, rep
