@@ -48,7 +48,7 @@ Timing: every measured call first runs back to back, untimed, for 0.3 s
 calls bracketed by HIP events on the stream the library launches on.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
-       [--no-cpu-baseline] [--no-secondary] [--copy-probe] [--mfma-probe]
+       [--no-cpu-baseline] [--no-secondary] [--copy-probe] [--mfma-probe] [--vendor-probe]
 """
 from __future__ import annotations
 
@@ -556,6 +556,47 @@ def copy_probe() -> None:
                       "GB_per_s_read_plus_write": 2 * nbytes / (ms * 1e-3) / 1e9}))
 
 
+def vendor_probe(steps: int = 50, warmup: int = 5, rounds: int = 2) -> None:
+    """Reference rates of the vendor BLAS on this GPU (hipBLASLt, reached
+    through torch.mm with out_dtype=float32 and torch._int_mm) for the square
+    products gemm_bf16_N8192_s32 (bfloat16 in, binary32 out) and
+    gemm_i8_N8192_s32 (int8 in, int32 out): the same device-resident inputs,
+    timed the same way and alternated with this library's tcu_gemm in one
+    process.  Context for the products' rates only -- nothing of the library
+    calls it.  Prints one JSON line."""
+    import torch
+    res = {"probe": "vendor BLAS reference (torch.mm / torch._int_mm -> hipBLASLt)",
+           "steps": steps, "warmup": warmup, "rounds": []}
+    for _ in range(rounds):
+        rnd = {}
+        for name in ("gemm_bf16_N8192_s32", "gemm_i8_N8192_s32"):
+            w = Workload(name)
+            w.tcu.tcu_set_unit(w.s)
+            N = w.spec["N"]
+            ours = time_steps(w.call, steps, warmup)
+            if w.spec["dtype"] == "bf16":
+                cv = torch.empty(N, N, dtype=torch.float32, device="cuda")
+                vendor_call = lambda: torch.mm(w.dA, w.dB, out_dtype=torch.float32, out=cv)  # noqa: E731
+            else:
+                holder = {}
+                vendor_call = lambda: holder.__setitem__("c", torch._int_mm(w.dA, w.dB))  # noqa: E731
+            vendor = time_steps(vendor_call, steps, warmup)
+            w.call()
+            vendor_call()
+            torch.cuda.synchronize()
+            ref = cv if w.spec["dtype"] == "bf16" else holder["c"]
+            diff = (w.C.double() - ref.double()).abs().max().item()
+            scale = ref.double().abs().max().item()
+            flops = 2.0 * N ** 3
+            rnd[name] = {"tcu_gemm_ms": ours, "vendor_ms": vendor,
+                         "tcu_gemm_T_per_s": flops / (ours * 1e-3) / 1e12,
+                         "vendor_T_per_s": flops / (vendor * 1e-3) / 1e12,
+                         "max_abs_difference": diff, "max_abs_value": scale}
+            del w
+        res["rounds"].append(rnd)
+    print(json.dumps(res), flush=True)
+
+
 def mfma_probe(iters: int = 100000, reps: int = 3) -> None:
     """The matrix cores' sustained rate on this chip with nothing else
     running (libtcu_probe.so: the product's persistent grid, one workgroup of
@@ -614,7 +655,82 @@ def mfma_probe(iters: int = 100000, reps: int = 3) -> None:
             res[f"{name}_{kind}"] = {"ms": ms, "T_per_s": rate, "frac_of_peak": rate / peak}
     res["overlap"] = overlap_probe(lib, blocks, st)
     res["lds"] = lds_probe(lib, blocks, st)
+    res["dma"] = dma_probe(lib, blocks, st)
+    res["pingpong"] = pingpong_probe(lib, blocks, st)
     print(json.dumps(res), flush=True)
+
+
+def _timed_launch(run, st, reps: int) -> float:
+    """Milliseconds per launch: one untimed launch, then `reps` between events."""
+    import torch
+    run()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(st)
+    for _ in range(reps):
+        run()
+    e1.record(st)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def dma_probe(lib, blocks: int, st, iters: int = 20000, reps: int = 3) -> dict:
+    """Rate of direct global -> LDS loads per CU (libtcu_probe.so,
+    tcu_probe_dma; one workgroup of 4, 8 or 16 waves per CU, each wave 4
+    loads of 1 KiB per round from a cache-resident window), in bytes per ns
+    per CU."""
+    import ctypes
+    import torch
+    fn = lib.tcu_probe_dma
+    fn.restype = ctypes.c_int
+    fn.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_int,
+                   ctypes.c_void_p]
+    src = torch.ones(1 << 18, dtype=torch.int32, device="cuda")      # 1 MiB (>= 512 KiB read)
+    out = torch.empty(blocks * 1024, dtype=torch.int32, device="cuda")
+    res = {"iters": iters}
+    for threads in (256, 512, 1024):
+        def run():
+            rc = fn(src.data_ptr(), out.data_ptr(), iters, blocks, threads, st.cuda_stream)
+            if rc != 0:
+                raise RuntimeError(f"dma probe launch failed ({rc})")
+        ms = _timed_launch(run, st, reps)
+        nbytes = (threads // 64) * iters * 4 * 1024          # per CU
+        res[f"waves{threads // 64}"] = {"ms": ms, "bytes_per_ns_per_cu": nbytes / (ms * 1e6)}
+    return res
+
+
+def pingpong_probe(lib, blocks: int, st, iters: int = 20000, reps: int = 3) -> dict:
+    """The full-tile product's two-group phase structure with its parts added
+    one at a time (libtcu_probe.so, tcu_probe_pingpong; one workgroup of 8
+    waves per CU, products from registers): nanoseconds per matrix-core
+    instruction per SIMD for no ping-pong, ping-pong with barriers only, +
+    the other group's fragment reads, + its DMA loads (the product's phase),
+    and the DMA loads without the reads."""
+    import ctypes
+    import torch
+    fn = lib.tcu_probe_pingpong
+    fn.restype = ctypes.c_int
+    fn.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                   ctypes.c_int, ctypes.c_void_p]
+    g = torch.Generator(device="cuda").manual_seed(79)
+    ops = torch.randn(blocks * 2048 * 8, generator=g, device="cuda").to(torch.bfloat16)
+    ops = ops.view(torch.int32)
+    assert ops.numel() == blocks * 2048 * 4
+    src = torch.zeros(1 << 18, dtype=torch.int32, device="cuda")     # 1 MiB
+    out = torch.empty(blocks * 512, dtype=torch.int32, device="cuda")
+    res = {"iters": iters}
+    names = ("no_pingpong", "pingpong_barriers", "plus_fragment_reads", "plus_dma_product_phase",
+             "dma_without_reads")
+    for mode, name in enumerate(names):
+        def run():
+            rc = fn(mode, ops.data_ptr(), src.data_ptr(), out.data_ptr(), iters, blocks,
+                    st.cuda_stream)
+            if rc != 0:
+                raise RuntimeError(f"pingpong probe launch failed ({rc})")
+        ms = _timed_launch(run, st, reps)
+        res[name] = {"ms": ms, "ns_per_product_per_simd": ms * 1e6 / (64 * iters)}
+    return res
 
 
 def lds_probe(lib, blocks: int, st, iters: int = 20000, reps: int = 3) -> dict:
@@ -713,6 +829,7 @@ def main() -> int:
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--copy-probe", action="store_true")
     ap.add_argument("--mfma-probe", action="store_true")
+    ap.add_argument("--vendor-probe", action="store_true")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -731,6 +848,9 @@ def main() -> int:
         return 0
     if args.mfma_probe:
         mfma_probe()
+        return 0
+    if args.vendor_probe:
+        vendor_probe()
         return 0
     known = {**inputs.WORKLOADS, **inputs.RECT_WORKLOADS, **inputs.POLY_WORKLOADS,
              **inputs.TC_WORKLOADS, **inputs.DFT_WORKLOADS}
