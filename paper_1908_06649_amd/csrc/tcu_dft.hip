@@ -22,8 +22,10 @@
 // enter as the sum of two bf16 words (hi + lo), and every real product is
 // formed as hi*hi + hi*lo + lo*hi into binary32 accumulators, about 2^-16
 // relative accuracy (one bf16 rounding would cost 2^-9 per level).  The
-// twiddles are computed in the kernel (sincospi of an exactly reduced
-// angle); nothing is precomputed or stored.
+// twiddles are computed in the kernel: for N_t <= 2^20 as the product of two
+// entries of per-workgroup LDS tables (each the sincospi of an exact angle),
+// above that as one sincospi of the exactly reduced angle; nothing is
+// stored between launches.
 #include <mutex>
 
 #include "tcu_device.h"
@@ -49,6 +51,45 @@ __device__ __forceinline__ f32x2 twiddle(int64_t m, int64_t N) {
 // Complex product of two (re, im) pairs.
 __device__ __forceinline__ f32x2 cmul(f32x2 a, f32x2 b) {
   return f32x2{a[0] * b[0] - a[1] * b[1], a[0] * b[1] + a[1] * b[0]};
+}
+
+// Twiddles of one level, N = 2^L: for L <= kTabLg,
+//   w_N^m = T_hi[m >> b] * T_lo[m mod 2^b],   b = ceil(L / 2),
+// T_lo[i] = w_N^i (i < 2^b) and T_hi[i] = w_N^(i 2^b) (i < 2^(L-b)), built
+// in LDS by the workgroup (2^b + 2^(L-b) <= 2048 sincospi evaluations, in
+// place of about three per lane and transform step); above kTabLg every
+// twiddle is one sincospi.  The choice depends on L alone, so every kernel
+// computes the same twiddle bit for bit.
+constexpr int kTabLg = 20;
+__host__ __device__ constexpr int tab_entries(int L) {
+  return L <= kTabLg ? (1 << ((L + 1) / 2)) + (1 << (L / 2)) : 0;
+}
+struct TwTab {
+  const f32x2 *lo = nullptr;   // LDS; null: no table
+  const f32x2 *hi = nullptr;
+  int b = 0;
+  int lg = 0;                  // L
+};
+// Fill pool[0 .. tab_entries(L)) (threads tid < nthreads share the work);
+// the caller synchronises the workgroup before the first lookup.
+__device__ __forceinline__ TwTab build_tab(f32x2 *pool, int L, int tid, int nthreads) {
+  TwTab t;
+  t.lg = L;
+  if (L > kTabLg) return t;
+  t.b = (L + 1) / 2;
+  const int nlo = 1 << t.b, nhi = 1 << (L - t.b);
+  const int64_t N = (int64_t)1 << L;
+  for (int i = tid; i < nlo + nhi; i += nthreads)
+    pool[i] = i < nlo ? twiddle(i, N) : twiddle((int64_t)(i - nlo) << t.b, N);
+  t.lo = pool;
+  t.hi = pool + nlo;
+  return t;
+}
+// w_N^(m mod N).
+__device__ __forceinline__ f32x2 tw(const TwTab &t, int64_t m) {
+  const int64_t mm = m & (((int64_t)1 << t.lg) - 1);
+  if (t.lo == nullptr) return twiddle(mm, (int64_t)1 << t.lg);
+  return cmul(t.hi[mm >> t.b], t.lo[mm & ((1 << t.b) - 1)]);
 }
 
 // Shapes of a radix-S step on the unit: a lane holds kRun consecutive
@@ -149,9 +190,9 @@ __device__ __forceinline__ void dft_half(const DftWeights<S> &W, const DftData<S
 }
 // Outputs k0 .. k0+3 of transform J times the twiddles w_(N_t)^(J k):
 // w^(J k0), then repeated products with step = w^J.
-__device__ __forceinline__ void dft_twiddle4(f32x2 (&y)[4], int64_t J, int k0, int lg_nt,
-                                             int64_t nt_mask, f32x2 step) {
-  f32x2 w = twiddle((J * k0) & nt_mask, (int64_t)1 << lg_nt);
+__device__ __forceinline__ void dft_twiddle4(f32x2 (&y)[4], int64_t J, int k0, const TwTab &tab,
+                                             f32x2 step) {
+  f32x2 w = tw(tab, J * k0);
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     y[i] = cmul(y[i], w);
@@ -167,15 +208,17 @@ __global__ __launch_bounds__(kDftThreads) void dft_level_kernel(
     int64_t ntrans) {
   constexpr int kRun = DftShape<S>::kRun, kH = DftShape<S>::kH;
   __shared__ f32x2 wtab[S];               // w_R^m, m < R
+  __shared__ f32x2 pool[tab_entries(kTabLg)];
 
   const int R = 1 << lg_r;
   const int lg_pv = lg_n - lg_r;          // log2 of the transforms per vector
   const int lg_nt = lg_n - lg_p;          // log2 N_t
-  const int64_t nt_mask = ((int64_t)1 << lg_nt) - 1;
   const bool last = lg_nt == lg_r;        // N_t = R: no twiddles
   const bool contiguous = lg_p == 0 && R >= 4;   // a lane's 4 outputs are adjacent
 
   if (threadIdx.x < (unsigned)R) wtab[threadIdx.x] = twiddle(threadIdx.x, R);
+  TwTab tab;
+  if (!last) tab = build_tab(pool, lg_nt, threadIdx.x, kDftThreads);
   __syncthreads();
 
   const int lane = threadIdx.x & 63;
@@ -207,7 +250,7 @@ __global__ __launch_bounds__(kDftThreads) void dft_level_kernel(
     dft_data<S>(X, xr, xi, sc);
     const int64_t J = c >> lg_p, K = c & (((int64_t)1 << lg_p) - 1);
     f32x2 *vout = dst + (b << lg_n) + ((J << lg_r) << lg_p) + K;
-    const f32x2 step = last ? f32x2{1.f, 0.f} : twiddle(J & nt_mask, (int64_t)1 << lg_nt);
+    const f32x2 step = last ? f32x2{1.f, 0.f} : tw(tab, J);
 #pragma unroll
     for (int h = 0; h < kH; ++h) {
       f32x4 re, im;
@@ -217,7 +260,7 @@ __global__ __launch_bounds__(kDftThreads) void dft_level_kernel(
       f32x2 y[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) y[i] = f32x2{re[i], im[i]};
-      if (!last) dft_twiddle4(y, J, k0, lg_nt, nt_mask, step);
+      if (!last) dft_twiddle4(y, J, k0, tab, step);
       if (contiguous) {   // outputs k0 .. k0+3 of transform J: 32 adjacent bytes
         f32x4 *o = (f32x4 *)(vout + k0);
         o[0] = f32x4{y[0][0], y[0][1], y[1][0], y[1][1]};
@@ -272,15 +315,20 @@ __global__ __launch_bounds__(kPairThreads) void dft_pair_kernel(
   constexpr int kRow = pair_row<S>(), kGrp = pair_group<S>();
   __shared__ f32x2 wtab[S];
   __shared__ f32x2 tile[kPairGroups * kGrp];
+  // level t's table (N_t <= 2^20) and level t+1's (N' = N_t / S), or one
+  // of them: at most 2^10 + 2^10 + 2^(10 - lg_s/2) + 2^(10 - lg_s/2) entries
+  constexpr int kPool = tab_entries(kTabLg) + tab_entries(kTabLg - (S == 32 ? 5 : 4));
+  __shared__ f32x2 pool[kPool];
 
   const int lg_nt = lg_n - lg_p;             // level t: N_t
   const int lg_n2 = lg_nt - lg_s;            // level t+1: N' = N_t / S
-  const int64_t nt_mask = ((int64_t)1 << lg_nt) - 1;
-  const int64_t n2_mask = ((int64_t)1 << lg_n2) - 1;
   const int lg_jp = lg_n2 - lg_s;            // log2 (N'/S): the J' range
   const int lg_pv = lg_n - lg_s;             // n / S: level t's element stride
 
   if (threadIdx.x < (unsigned)S) wtab[threadIdx.x] = twiddle(threadIdx.x, S);
+  const TwTab tab1 = build_tab(pool, lg_nt, threadIdx.x, kPairThreads);
+  TwTab tab2;
+  if (!last2) tab2 = build_tab(pool + tab_entries(lg_nt), lg_n2, threadIdx.x, kPairThreads);
   __syncthreads();
   const int lane = threadIdx.x & 63;
   const int r = lane & 15, g = lane >> 4;
@@ -321,7 +369,7 @@ __global__ __launch_bounds__(kPairThreads) void dft_pair_kernel(
       }
       DftData<S> X;
       dft_data<S>(X, xr, xi, sc);
-      const f32x2 step = twiddle(J & nt_mask, (int64_t)1 << lg_nt);
+      const f32x2 step = tw(tab1, J);
 #pragma unroll
       for (int h = 0; h < kH; ++h) {
         f32x4 re, im;
@@ -330,7 +378,7 @@ __global__ __launch_bounds__(kPairThreads) void dft_pair_kernel(
         f32x2 y[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) y[e] = f32x2{re[e], im[e]};
-        dft_twiddle4(y, J, k0, lg_nt, nt_mask, step);
+        dft_twiddle4(y, J, k0, tab1, step);
         f32x2 *t = tile + r * kGrp + jp * kRow + k0;
 #pragma unroll
         for (int e = 0; e < 4; ++e) t[e] = y[e];
@@ -363,7 +411,7 @@ __global__ __launch_bounds__(kPairThreads) void dft_pair_kernel(
       DftData<S> X;
       dft_data<S>(X, xr, xi, sc);
       f32x2 *vout = vdst + ((J2 << lg_s) << (lg_p + lg_s)) + K2;
-      const f32x2 step = last2 ? f32x2{1.f, 0.f} : twiddle(J2 & n2_mask, (int64_t)1 << lg_n2);
+      const f32x2 step = last2 ? f32x2{1.f, 0.f} : tw(tab2, J2);
 #pragma unroll
       for (int h = 0; h < kH; ++h) {
         f32x4 re, im;
@@ -372,7 +420,7 @@ __global__ __launch_bounds__(kPairThreads) void dft_pair_kernel(
         f32x2 y[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) y[e] = f32x2{re[e], im[e]};
-        if (!last2) dft_twiddle4(y, J2, k0, lg_n2, n2_mask, step);
+        if (!last2) dft_twiddle4(y, J2, k0, tab2, step);
 #pragma unroll
         for (int e = 0; e < 4; ++e) vout[(int64_t)(k0 + e) << (lg_p + lg_s)] = y[e];
       }
