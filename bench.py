@@ -736,8 +736,9 @@ def pingpong_probe(lib, blocks: int, st, iters: int = 20000, reps: int = 3) -> d
 def lds_probe(lib, blocks: int, st, iters: int = 20000, reps: int = 3) -> dict:
     """LDS read rate per CU (libtcu_probe.so, tcu_probe_lds; one workgroup of
     4, 8 or 16 waves per CU, 16 reads per wave and round): ds_read_b128 (1 KiB
-    per instruction) and ds_read_b64_tr_b16 (512 bytes), in bytes per ns per
-    CU and ns per instruction per CU."""
+    per instruction), ds_read_b64_tr_b16 and ds_read_b64_tr_b8 (512 bytes;
+    the 16-bit and int8 products' weights reads), in bytes per ns per CU and
+    ns per instruction per CU."""
     import ctypes
     import torch
     fn = lib.tcu_probe_lds
@@ -746,7 +747,7 @@ def lds_probe(lib, blocks: int, st, iters: int = 20000, reps: int = 3) -> dict:
                    ctypes.c_void_p]
     out = torch.empty(blocks * 1024, dtype=torch.int32, device="cuda")
     res = {"iters": iters}
-    for kind, name, nbytes in ((0, "b128", 1024), (1, "tr16_b64", 512)):
+    for kind, name, nbytes in ((0, "b128", 1024), (1, "tr16_b64", 512), (2, "tr8_b64", 512)):
         for threads in (256, 512, 1024):
             def run():
                 rc = fn(kind, out.data_ptr(), iters, blocks, threads, st.cuda_stream)

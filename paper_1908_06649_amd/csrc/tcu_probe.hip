@@ -129,8 +129,9 @@ overlap_probe_kernel(const u32x4 *__restrict__ ops, int64_t iters, unsigned *__r
 // LDS read-rate probe: every wave of a workgroup (4, 8 or 16 waves, one
 // workgroup per CU) reads 1 KiB per instruction with
 // ds_read_b128 (kKind 0; 64 lanes x 16 contiguous bytes, conflict-free) or
-// 512 bytes per instruction with ds_read_b64_tr_b16 (kKind 1; 64 lanes x 8
-// contiguous bytes), 16 instructions per round over a 64 KiB region, the
+// 512 bytes per instruction with ds_read_b64_tr_b16 (kKind 1) or
+// ds_read_b64_tr_b8 (kKind 2; 64 lanes x 8 contiguous bytes each), 16
+// instructions per round over a 64 KiB region, the
 // offset moving every round so that no read can be hoisted; the values are
 // folded into one word per lane.
 template <int kKind>
@@ -148,7 +149,7 @@ __global__ __launch_bounds__(1024) void lds_probe_kernel(unsigned *__restrict__ 
       if constexpr (kKind == 0) {
         acc ^= *(const u32x4 *)(s + off + 16 * lane);
       } else {
-        const u32x2 v = lds_read_tr16(s + off + 8 * lane);
+        const u32x2 v = kKind == 1 ? lds_read_tr16(s + off + 8 * lane) : lds_read_tr8(s + off + 8 * lane);
         acc[0] ^= v[0];
         acc[1] ^= v[1];
       }
@@ -344,7 +345,7 @@ extern "C" __attribute__((visibility("default"))) int tcu_probe_overlap(int mode
 }
 
 // out: blocks * threads words (device).  kind 0: ds_read_b128, 1:
-// ds_read_b64_tr_b16; threads 256, 512 or 1024.  Every wave issues
+// ds_read_b64_tr_b16, 2: ds_read_b64_tr_b8; threads 256, 512 or 1024.  Every wave issues
 // 16 * iters LDS read instructions.  Asynchronous on `stream`.  Returns 0,
 // or -1 for bad arguments, -6 for a launch error.
 extern "C" __attribute__((visibility("default"))) int tcu_probe_lds(int kind, void *out,
@@ -358,6 +359,8 @@ extern "C" __attribute__((visibility("default"))) int tcu_probe_lds(int kind, vo
     hipLaunchKernelGGL(tcu::lds_probe_kernel<0>, dim3(blocks), dim3(threads), 0, st, u, iters);
   else if (kind == 1)
     hipLaunchKernelGGL(tcu::lds_probe_kernel<1>, dim3(blocks), dim3(threads), 0, st, u, iters);
+  else if (kind == 2)
+    hipLaunchKernelGGL(tcu::lds_probe_kernel<2>, dim3(blocks), dim3(threads), 0, st, u, iters);
   else
     return -1;
   return hipGetLastError() == hipSuccess ? 0 : -6;
