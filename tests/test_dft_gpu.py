@@ -33,10 +33,13 @@ def run_dft(x: torch.Tensor, s: int, with_work: bool = True) -> np.ndarray:
     return y.view(batch, n).cpu().numpy()
 
 
-SIZES = [1, 2, 4, 8, 16, 32, 64, 128, 512, 1024, 2048, 4096, 32768, 65536, 1 << 20]
+# 2^21 and 2^23: levels with N_t above 2^20, whose twiddles are single
+# sincospi evaluations rather than products of two table entries
+SIZES = [1, 2, 4, 8, 16, 32, 64, 128, 512, 1024, 2048, 4096, 32768, 65536, 1 << 20, 1 << 21,
+         1 << 23]
 
 
-# one vector of 2^20 per unit size here; the workload test runs a batch of them
+# one vector of 2^20 or more per unit size here; the workload test runs a batch of them
 CASES = [(n, b) for n in SIZES for b in (1, 3) if n < 1 << 20 or b == 1]
 
 
@@ -101,9 +104,12 @@ def test_dft_workload(name):
 # Sizes where two consecutive full-radix levels run as one launch: for s = 32
 # the first two levels from n = 2^14 (16 groups J' per vector) and levels 3-4
 # at n = 2^20 (P = 2^10); for s = 16 from n = 2^12, and levels 2-3 at
-# n = 2^16 (P = 16).
+# n = 2^16 (P = 16).  At n = 2^21 (s = 32) and 2^22 (s = 16) the first
+# level's N_t is above 2^20 (twiddles by sincospi) and the second's below
+# (twiddles from the tables).
 PAIR_CASES = [(1 << 12, 3, 16), (1 << 14, 2, 16), (1 << 16, 2, 16), (1 << 14, 3, 32),
-              (1 << 15, 2, 32), (1 << 20, 2, 32), (1 << 18, 1, 16)]
+              (1 << 15, 2, 32), (1 << 20, 2, 32), (1 << 18, 1, 16), (1 << 21, 1, 32),
+              (1 << 22, 1, 16)]
 
 
 @pytest.mark.parametrize("n,batch,s", PAIR_CASES)
