@@ -76,9 +76,10 @@ PROFILES = os.path.join(ROOT, "profiles")
 
 
 def kernel_sources(kind: str):
-    main = {"gemm": ["tcu_gemm.hip"], "rect": ["tcu_gemm.hip"],
+    main = {"gemm": ["tcu_gemm.hip", "tcu_tc_diag.h"], "rect": ["tcu_gemm.hip", "tcu_tc_diag.h"],
             "poly": ["tcu_poly.hip", "tcu_split.h"],
-            "tc": ["tcu_tc.hip", "tcu_gemm.hip"], "dft": ["tcu_dft.hip", "tcu_split.h"],
+            "tc": ["tcu_tc.hip", "tcu_gemm.hip", "tcu_tc_diag.h"],
+            "dft": ["tcu_dft.hip", "tcu_split.h"],
             "probe": ["tcu_probe.hip"]}.get(kind, ["tcu_tall.hip"])
     return [os.path.join(CSRC, f) for f in (*main, "tcu_device.h")]
 

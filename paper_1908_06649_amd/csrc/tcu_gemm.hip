@@ -29,6 +29,7 @@
 // Workgroup order is XCD-aware (see map_tile).
 #include "tcu_device.h"
 #include "tcu_launch.h"
+#include "tcu_tc_diag.h"
 
 namespace tcu {
 namespace {
@@ -350,7 +351,7 @@ __global__ __attribute__((amdgpu_flat_work_group_size(512, 512), amdgpu_waves_pe
 gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restrict__ B,
                unsigned char *__restrict__ C, int K, int64_t lda, int64_t ldb, int64_t ldc,
                int accum, int tiles_m, int tiles_n, int full, int nsplit, int m_lim,
-               int n_lim, TileRemap remap) {
+               int n_lim, TileRemap remap, int diag_pid) {
   constexpr bool kI8 = (in_bytes(DT) == 1);
   constexpr int ES = in_bytes(DT);
   constexpr int OB = out_bytes(DT);
@@ -390,7 +391,14 @@ gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restr
   const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int grp = wid >> 2, q = wid & 3;
   const int r = lane & 15, g = lane >> 4;
-  int item = blockIdx.x;
+  // With diag_pid >= 0 (the closure's D update, which also closes the next
+  // pivot band's diagonal block -- a tile of this launch): workgroup 0 takes
+  // that tile alone and then closes the block (close_diag_block, 512
+  // threads) while the others share the remaining tiles, skipping it.
+  const bool with_diag = DT == TCU_I8_BOOL && diag_pid >= 0;
+  const int stride = with_diag ? (int)gridDim.x - 1 : (int)gridDim.x;
+  const int limit = with_diag ? total - 1 : total;
+  int item = with_diag ? (int)blockIdx.x - 1 : (int)blockIdx.x;   // -1: the diagonal tile
   int m0, n0, nk;
   int tail_t = -1;   // item-relative index of a partial last stage, if the item holds it
   // This wave's DMA share of a stage: group 0 -> A blocks 4q..4q+3 (16 rows
@@ -439,6 +447,7 @@ gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restr
   bool split_item = false;   // the current item is a K slice (atomic epilogue)
   auto place = [&](int w) {
     int pid = w, slice = 0;
+    if (with_diag) pid = w < 0 ? diag_pid : (w < diag_pid ? w : w + 1);
     split_item = nsplit > 1 && w >= full;
     if (split_item) {
       int v = w - full;
@@ -628,8 +637,8 @@ gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restr
       // row: the 16 rows one store instruction touches land in distinct
       // banks, and a row's chunks are still one 256-byte row.
       const int em0 = m0, en0 = n0;
-      if (item + (int)gridDim.x < total) {
-        item += gridDim.x;
+      if (item >= 0 && item + stride < limit) {
+        item += stride;
         place(item);
         for (int s0 = 0; s0 < kRing; ++s0)
           if (s0 < nk) issue(s0, s0);
@@ -765,8 +774,18 @@ gemm_pp_kernel(const unsigned char *__restrict__ A, const unsigned char *__restr
     }
     // Every wave finished reading the ring at the last barrier of the loop.
     if (next_issued) continue;
-    item += gridDim.x;
-    if (item >= total) break;
+    if constexpr (DT == TCU_I8_BOOL) {
+      if (with_diag && item < 0) {
+        // The block's update is stored (the epilogue ends with a workgroup
+        // barrier, which orders the stores before the loads below); the ring
+        // is free.
+        close_diag_block<true, 512>(C + (int64_t)m0 * ldc_b + n0, ldc_b, kDiagBand,
+                                    *reinterpret_cast<DiagShared *>(smem));
+        break;
+      }
+    }
+    item += stride;
+    if (item >= limit) break;
     place(item);
     for (int s0 = 0; s0 < kRing; ++s0)
       if (s0 < nk) issue(s0, s0);
@@ -1140,7 +1159,7 @@ hipError_t launch_dt(const RectArgs &a, hipStream_t stream, int num_cus) {
     hipLaunchKernelGGL((gemm_pp_kernel<DT, kRingStages, false>), dim3(grid), dim3(512), 0, stream,
                        (const unsigned char *)a.A, (const unsigned char *)a.B,
                        (unsigned char *)a.C, (int)a.K, a.lda, a.ldb, a.ldc, a.accum ? 1 : 0,
-                       tm, tn, full, nsplit, (int)a.M, (int)a.N, TileRemap{});
+                       tm, tn, full, nsplit, (int)a.M, (int)a.N, TileRemap{}, -1);
     return hipGetLastError();
   }
   // Ragged shapes (dimensions that are not multiples of the tile or of a
@@ -1178,7 +1197,7 @@ hipError_t launch_dt(const RectArgs &a, hipStream_t stream, int num_cus) {
     hipLaunchKernelGGL((gemm_pp_kernel<DT, kRingStages, true>), dim3(grid), dim3(512), 0, stream,
                        (const unsigned char *)a.A, (const unsigned char *)a.B,
                        (unsigned char *)a.C, (int)a.K, a.lda, a.ldb, a.ldc, a.accum ? 1 : 0,
-                       tm, tn, full, nsplit, (int)a.M, (int)a.N, TileRemap{});
+                       tm, tn, full, nsplit, (int)a.M, (int)a.N, TileRemap{}, -1);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || edges_in_kernel) return e;
     if (a.M > M0) {
@@ -1232,7 +1251,7 @@ hipError_t launch_tc_panels(unsigned char *X, int64_t ld, int n, int k0, int Bk,
 }
 
 hipError_t launch_tc_rest(unsigned char *X, int64_t ld, int n, int k0, int Bk,
-                          hipStream_t stream, int num_cus) {
+                          hipStream_t stream, int num_cus, bool close_next) {
   const unsigned char *L = X + k0;
   const unsigned char *R = X + (int64_t)k0 * ld;
   // Whole 256-wide bands and 16-byte rows: the full-tile kernel over
@@ -1241,7 +1260,17 @@ hipError_t launch_tc_rest(unsigned char *X, int64_t ld, int n, int k0, int Bk,
     TileRemap rm;
     rm.band_n = k0 / 256;
     rm.skip_n = 256;
-    return launch_tc_tiles(X, ld, n, k0, n / 256, n / 256 - 1, rm, stream, num_cus);
+    const int tiles_m = n / 256, tiles_n = n / 256 - 1;
+    int diag_pid = -1;
+    if (close_next) {
+      // The next band's diagonal tile: tile row b + 1 and, the band's column
+      // b being skipped, grid column b; its index in map_tile's order.
+      const int tm = k0 / 256 + 1, tn = k0 / 256;
+      const int first_m = tm / kGroupM * kGroupM;
+      const int gsz = tiles_m - first_m < kGroupM ? tiles_m - first_m : kGroupM;
+      diag_pid = first_m * tiles_n + tn * gsz + (tm - first_m);
+    }
+    return launch_tc_tiles(X, ld, n, k0, tiles_m, tiles_n, rm, stream, num_cus, diag_pid);
   }
   if (ld % 16 == 0)
     return launch_bool<128, 128, true>(L, R, X, ld, n, n, Bk, k0, false, true, stream);
@@ -1254,7 +1283,7 @@ bool tc_full_tiles(int64_t n, int Bk, int64_t ld) {
 
 hipError_t launch_tc_tiles(unsigned char *X, int64_t ld, int n, int k0, int tiles_m,
                            int tiles_n, const TileRemap &remap, hipStream_t stream,
-                           int num_cus) {
+                           int num_cus, int diag_pid) {
   // The D formula X[I, J] |= X[I, band] X[band, J] (band = [k0, k0 + 256))
   // on a tiles_m x tiles_n grid of 256 x 256 tiles placed by remap, by at
   // most num_cus persistent workgroups.
@@ -1264,7 +1293,7 @@ hipError_t launch_tc_tiles(unsigned char *X, int64_t ld, int n, int k0, int tile
   hipLaunchKernelGGL((gemm_pp_kernel<TCU_I8_BOOL, 3, false>), dim3(grid), dim3(512), 0,
                      stream,
                      X + k0, X + (int64_t)k0 * ld, X, 256, ld, ld, ld, 1, tiles_m, tiles_n,
-                     tiles_m * tiles_n, 1, n, n, remap);
+                     tiles_m * tiles_n, 1, n, n, remap, diag_pid);
   return hipGetLastError();
 }
 

@@ -52,14 +52,19 @@ hipError_t launch_tc(unsigned char *X, int64_t ld, int64_t n, hipStream_t stream
 // (tcu_gemm.hip).
 hipError_t launch_tc_panels(unsigned char *X, int64_t ld, int n, int k0, int Bk,
                             hipStream_t stream);
+// close_next: the band's D update also closes the next band's diagonal
+// block [k0 + Bk, k0 + 2 Bk)^2 (whole 256-wide bands on the full-tile
+// kernel only).
 hipError_t launch_tc_rest(unsigned char *X, int64_t ld, int n, int k0, int Bk,
-                          hipStream_t stream, int num_cus);
+                          hipStream_t stream, int num_cus, bool close_next);
 // Whether the full-tile kernel takes the D updates (n a multiple of 256,
 // whole bands, 16-byte row pitch), and its launch on a remapped tile grid.
 bool tc_full_tiles(int64_t n, int Bk, int64_t ld);
+// diag_pid >= 0: the tile (in the kernel's tile order) that is the next
+// band's diagonal block, closed after its update; -1: none.
 hipError_t launch_tc_tiles(unsigned char *X, int64_t ld, int n, int k0, int tiles_m,
                            int tiles_n, const TileRemap &remap, hipStream_t stream,
-                           int num_cus);
+                           int num_cus, int diag_pid = -1);
 
 // Forward DFT of `batch` complex64 vectors of length n (a power of two):
 // ceil(log_s n) Cooley-Tukey levels alternating between work and y, the last
