@@ -19,7 +19,10 @@
 //   * per band [k0, k0 + Bk):
 //       diag  -- one workgroup: the block as 256-bit rows in registers, the
 //                iterative algorithm over the block's pivots by sub-bands
-//                of 32 (see tc_diag_kernel);
+//                of 32 (close_diag_block in tcu_tc_diag.h); a launch of its
+//                own for the first band and, with whole 256-wide bands,
+//                done for every later band by one workgroup of the previous
+//                band's rest launch, right after it updated the block;
 //       panels, rest -- the product kernels with the 0/1 output: the
 //                pivot column band, then the pivot row band and the rest
 //                in one launch (tcu_gemm.hip explains why the in-place
@@ -103,7 +106,8 @@ hipError_t launch_tc(unsigned char *X, int64_t ld, int64_t n, hipStream_t stream
     if (!diag_closed) TCU_TRY(launch_diag(X, ld, k0, Bk, vec, stream));
     if (n == Bk) break;
     TCU_TRY(launch_tc_panels(X, ld, (int)n, (int)k0, Bk, stream));
-    const bool close_next = vec && tc_full_tiles(n, Bk, ld) && k0 + kBand < n &&
+    // (the fused closure needs a second workgroup for the other tiles)
+    const bool close_next = vec && num_cus >= 2 && tc_full_tiles(n, Bk, ld) && k0 + kBand < n &&
                             tc_full_tiles(n, (int)(n - k0 - kBand < kBand ? n - k0 - kBand : kBand), ld);
     TCU_TRY(launch_tc_rest(X, ld, (int)n, (int)k0, Bk, stream, num_cus, close_next));
     diag_closed = close_next;
