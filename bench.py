@@ -94,7 +94,9 @@ def kernel_hash(kind: str) -> str:
 
 def counted_traffic(name: str, kind: str):
     """HBM bytes per launch from the committed rocprofv3 counter summary of
-    this workload, if it was taken on the current kernel source; else None."""
+    this workload, if it was taken on the current kernel source; else None.
+    A workload whose call is several launches (the closure) has a summary
+    with a per-call total, which is what its per-call rate compares with."""
     path = os.path.join(PROFILES, f"{name}_counters.txt")
     if not os.path.exists(path):
         return None
@@ -107,7 +109,7 @@ def counted_traffic(name: str, kind: str):
     if fields.get("kernel_source_sha256") != kernel_hash(kind):
         return None
     try:
-        return float(fields["hbm_bytes_per_dispatch"])
+        return float(fields.get("hbm_bytes_per_call", fields["hbm_bytes_per_dispatch"]))
     except (KeyError, ValueError):
         return None
 

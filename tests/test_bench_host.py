@@ -121,3 +121,29 @@ def test_host_info_fields():
     h = bench.host_info()
     assert {"cpu_model", "nproc", "OMP_NUM_THREADS", "oracle_threads"} <= set(h)
     assert h["nproc"] >= 1 and h["oracle_threads"] >= 1
+
+
+def test_counted_traffic_reads_the_summaries():
+    """Every counter summary under profiles/ parses; the bench takes its traffic
+    only from one taken on the current kernel source, and for a call made of
+    several launches (the closure) the per-call total."""
+    import glob
+    import os
+    import re
+    kinds = {"gemm": "gemm", "tall": "tall", "cor1": "rect", "pad": "rect", "poly": "poly",
+             "tc": "tc", "dft": "dft"}
+    paths = sorted(glob.glob(os.path.join(bench.PROFILES, "*_counters.txt")))
+    assert paths
+    for path in paths:
+        name = os.path.basename(path)[:-len("_counters.txt")]
+        kind = kinds[name.split("_")[0]]
+        text = open(path).read()
+        digest = re.search(r"^kernel_source_sha256: (\S+)", text, re.M).group(1)
+        got = bench.counted_traffic(name, kind)
+        if digest != bench.kernel_hash(kind):
+            assert got is None
+            continue
+        per_call = re.search(r"^hbm_bytes_per_call: (\S+)", text, re.M)
+        want = per_call or re.search(r"^hbm_bytes_per_dispatch: (\S+)", text, re.M)
+        assert got == float(want.group(1))
+        assert got > 0
