@@ -365,8 +365,9 @@ const char *tcu_strerror(int status);
  *     persistent kernel wherever its shape conditions hold),
  *     TCU_PATH_GENERAL (the general kernel), TCU_PATH_RING (the small-tile
  *     ring kernel where its shape conditions hold).
- *   TCU_KNOB_PP_GRID: workgroups of the persistent full-tile kernel (0: one
- *     per compute unit).
+ *   TCU_KNOB_PP_GRID: workgroups of the persistent full-tile kernel, in the
+ *     products and in the transitive closure's D updates (0: one per compute
+ *     unit).
  *   TCU_KNOB_SPLIT_K: forced number of contracted-index ranges of a
  *     full-tile product with binary32/int32 output (0: by size).
  *   TCU_KNOB_TAIL_SPLIT: forced number of ranges of the last round's tiles

@@ -100,6 +100,9 @@ hipError_t launch_tc(unsigned char *X, int64_t ld, int64_t n, hipStream_t stream
   // band's diagonal block (one workgroup, right after updating that block,
   // while the others update the rest), so only the first band's closure is
   // a launch of its own.
+  // Workgroups of the persistent D-update launch: one per CU, or the test
+  // override TCU_KNOB_PP_GRID (a tiny grid gives every workgroup many tiles).
+  const int pp_grid = knob(TCU_KNOB_PP_GRID) > 0 ? knob(TCU_KNOB_PP_GRID) : num_cus;
   bool diag_closed = false;
   for (int64_t k0 = 0; k0 < n; k0 += kBand) {
     const int Bk = (int)(n - k0 < kBand ? n - k0 : kBand);
@@ -107,9 +110,9 @@ hipError_t launch_tc(unsigned char *X, int64_t ld, int64_t n, hipStream_t stream
     if (n == Bk) break;
     TCU_TRY(launch_tc_panels(X, ld, (int)n, (int)k0, Bk, stream));
     // (the fused closure needs a second workgroup for the other tiles)
-    const bool close_next = vec && num_cus >= 2 && tc_full_tiles(n, Bk, ld) && k0 + kBand < n &&
+    const bool close_next = vec && pp_grid >= 2 && tc_full_tiles(n, Bk, ld) && k0 + kBand < n &&
                             tc_full_tiles(n, (int)(n - k0 - kBand < kBand ? n - k0 - kBand : kBand), ld);
-    TCU_TRY(launch_tc_rest(X, ld, (int)n, (int)k0, Bk, stream, num_cus, close_next));
+    TCU_TRY(launch_tc_rest(X, ld, (int)n, (int)k0, Bk, stream, pp_grid, close_next));
     diag_closed = close_next;
   }
   return hipSuccess;

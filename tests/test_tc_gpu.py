@@ -51,6 +51,18 @@ def test_tc_random_graphs(n, deg):
     assert np.array_equal(run_tc(d), oracle.transitive_closure(d))
 
 
+# The D update of each band also closes the next band's diagonal block in
+# its workgroup 0 while the others take the remaining tiles; with a tiny
+# persistent grid every other workgroup walks many tiles around that one
+# (grid 2: workgroup 1 takes them all; grid 1: no fused closure).
+@pytest.mark.parametrize("grid", [1, 2, 3, 7, 29])
+@pytest.mark.parametrize("n", [512, 1280, 2048])
+def test_tc_fused_diagonal_small_grids(n, grid, knobs):
+    knobs(tcu.TCU_KNOB_PP_GRID, grid)
+    d = graph(n, 1.1, n + grid)
+    assert np.array_equal(run_tc(d), oracle.transitive_closure(d))
+
+
 @pytest.mark.parametrize("n,ld", [(300, 304), (300, 301), (513, 528), (700, 777), (1000, 1024)])
 def test_tc_pitched(n, ld):
     d = graph(n, 1.2, n + ld)
