@@ -559,7 +559,7 @@ def copy_probe() -> None:
                       "GB_per_s_read_plus_write": 2 * nbytes / (ms * 1e-3) / 1e9}))
 
 
-def vendor_probe(steps: int = 50, warmup: int = 5, rounds: int = 2) -> None:
+def vendor_probe(steps: int = 50, warmup: int = 5, passes: int = 2) -> None:
     """Reference rates of the vendor BLAS on this GPU (hipBLASLt, reached
     through torch.mm with out_dtype=float32 and torch._int_mm) for the square
     products gemm_bf16_N8192_s32 (bfloat16 in, binary32 out) and
@@ -569,9 +569,9 @@ def vendor_probe(steps: int = 50, warmup: int = 5, rounds: int = 2) -> None:
     calls it.  Prints one JSON line."""
     import torch
     res = {"probe": "vendor BLAS reference (torch.mm / torch._int_mm -> hipBLASLt)",
-           "steps": steps, "warmup": warmup, "rounds": []}
-    for _ in range(rounds):
-        rnd = {}
+           "steps": steps, "warmup": warmup, "passes": []}
+    for _ in range(passes):
+        one = {}
         for name in ("gemm_bf16_N8192_s32", "gemm_i8_N8192_s32"):
             w = Workload(name)
             w.tcu.tcu_set_unit(w.s)
@@ -591,12 +591,12 @@ def vendor_probe(steps: int = 50, warmup: int = 5, rounds: int = 2) -> None:
             diff = (w.C.double() - ref.double()).abs().max().item()
             scale = ref.double().abs().max().item()
             flops = 2.0 * N ** 3
-            rnd[name] = {"tcu_gemm_ms": ours, "vendor_ms": vendor,
+            one[name] = {"tcu_gemm_ms": ours, "vendor_ms": vendor,
                          "tcu_gemm_T_per_s": flops / (ours * 1e-3) / 1e12,
                          "vendor_T_per_s": flops / (vendor * 1e-3) / 1e12,
                          "max_abs_difference": diff, "max_abs_value": scale}
             del w
-        res["rounds"].append(rnd)
+        res["passes"].append(one)
     print(json.dumps(res), flush=True)
 
 
